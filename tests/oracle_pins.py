@@ -1,0 +1,276 @@
+"""Pins for the CPU oracle: checks against what the paper and the mathematics fix.
+
+Each pin takes the oracle module as an argument and raises AssertionError when
+the oracle disagrees with a fact that does not come from the oracle itself:
+hand-derived fixtures under tests/golden/ (each cites the passage it follows),
+closed forms, invariants the repair rule implies, exact no-op cases, and a
+property proved from the definitions (idempotence under a stated condition).
+``test_oracle_mutants.py`` runs the whole battery on deliberately broken copies
+of the oracle and requires every copy to fail at least one pin.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _one_hot_keys(one_hot_of, d):
+    K = np.zeros((len(one_hot_of), d), dtype=np.float32)
+    K[np.arange(len(one_hot_of)), one_hot_of] = 1.0
+    return K
+
+
+# ----------------------------------------------------------------------------
+# Eq. 1 / twin rule / Eq. 4
+# ----------------------------------------------------------------------------
+def pin_closed_forms(o):
+    fx = _load("closed_forms.json")
+    K = np.asarray(fx["keys"], dtype=np.float32)
+    for case in fx["cases"]:
+        r = o.nn_scores(K, "f32", None, case["w"])
+        np.testing.assert_allclose(r["best_all"], case["best"], rtol=0, atol=1e-12)
+        np.testing.assert_array_equal(r["arg_all"], case["arg"])
+        np.testing.assert_allclose(r["second_all"], case["second"], rtol=0, atol=1e-12)
+
+
+def pin_window_and_sentinel(o):
+    fx = _load("window_boundary.json")
+    K = _one_hot_keys(fx["one_hot_of"], fx["d"])
+    ret = np.asarray(fx["retained"], dtype=np.uint8)
+    r = o.nn_scores(K, "f32", ret, fx["w"])
+    np.testing.assert_array_equal(r["best_all"], fx["best_all"])
+    np.testing.assert_array_equal(r["arg_all"], fx["arg_all"])
+    np.testing.assert_array_equal(r["best_ret"], fx["best_ret"])
+    np.testing.assert_array_equal(r["arg_ret"], fx["arg_ret"])
+    sh = fx["short"]
+    r = o.nn_scores(K[: sh["n"]], "f32", np.ones(sh["n"], np.uint8), sh["w"])
+    for k in ("best_all", "best_ret"):
+        np.testing.assert_array_equal(r[k], sh["best"])
+    for k in ("arg_all", "arg_ret"):
+        np.testing.assert_array_equal(r[k], sh["arg"])
+    iw = fx["inside_window"]
+    only = np.zeros(iw["n"], np.uint8)
+    only[iw["retained_only"]] = 1
+    r = o.nn_scores(K[: iw["n"]], "f32", only, iw["w"], rows=np.array([iw["row"]]))
+    assert r["best_ret"][0] == iw["best"] and r["arg_ret"][0] == iw["arg"]
+
+
+def pin_scale_invariance(o):
+    """Eq. 1 depends on directions only: positive per-key rescaling leaves every output unchanged."""
+    g = np.random.Generator(np.random.PCG64(7))
+    K = g.standard_normal((40, 8))
+    K[5] = 2.5 * K[30]                        # an exact scaled twin
+    ret = (g.random(40) < 0.5).astype(np.uint8)
+    a = o.nn_scores(K.astype(np.float32), "f32", ret, 3)
+    scale = 2.0 ** g.integers(-6, 7, size=40)  # powers of two keep the float32 inputs exact
+    b = o.nn_scores((K * scale[:, None]).astype(np.float32), "f32", ret, 3)
+    for k in ("best_all", "best_ret"):
+        np.testing.assert_allclose(a[k], b[k], rtol=0, atol=1e-12)
+    assert abs(a["best_all"][5] - 1.0) < 1e-12 and a["arg_all"][5] == 30
+    # the same pair seen from the other side: symmetry of Eq. 1
+    assert abs(a["best_all"][30] - 1.0) < 1e-12 and a["arg_all"][30] == 5
+
+
+def pin_bf16_decode(o):
+    """Raw bf16 bits decode exactly: 0x3F80 = 1.0, 0xC000 = -2.0, 0x4040 = 3.0."""
+    bits = np.array([[0x3F80, 0, 0, 0], [0xC000, 0, 0, 0], [0, 0x4040, 0, 0], [0x4040, 0, 0, 0]],
+                    dtype=np.uint16)
+    r = o.nn_scores(bits, "bf16", None, 0)
+    np.testing.assert_allclose(r["best_all"], [1.0, 0.0, 0.0, 1.0], atol=1e-15)
+    np.testing.assert_array_equal(r["arg_all"], [3, 2, 0, 0])
+
+
+def pin_nonfinite_rejected(o):
+    K = np.ones((4, 4), np.float32)
+    K[2, 1] = np.nan
+    try:
+        o.nn_scores(K, "f32", None, 0)
+    except ValueError:
+        return
+    raise AssertionError("non-finite keys were accepted")
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.4 repair
+# ----------------------------------------------------------------------------
+def pin_repair_ranked(o):
+    fx = _load("repair_ranked.json")
+    s0 = np.asarray(fx["s0"], dtype=np.uint8)
+    for case in fx["cases"]:
+        r = o.repair(np.asarray(case["b"]), s0, fx["tau"], fx["n_sink"], fx["n_recent"])
+        np.testing.assert_array_equal(r["orphans_ranked"], case["orphans_ranked"])
+        np.testing.assert_array_equal(r["donors_ranked"], case["donors_ranked"])
+        assert r["m"] == case["m"], (case["name"], r["m"])
+        np.testing.assert_array_equal(r["s1"], case["s1"])
+
+
+def pin_oscillation(o):
+    fx = _load("repair_oscillation.json")
+    K = _one_hot_keys(fx["one_hot_of"], fx["d"])
+    s = np.asarray(fx["s0"], dtype=np.uint8)
+    for step in ("pass1", "pass2"):
+        exp = fx[step]
+        r = o.repair_problem(K, "f32", s, int(s.sum()), fx["tau"], fx["w"], fx["n_sink"], fx["n_recent"])
+        np.testing.assert_array_equal(r["best_ret"], exp["b"])
+        np.testing.assert_array_equal(r["orphans_ranked"], exp["orphans_ranked"])
+        np.testing.assert_array_equal(r["donors_ranked"], exp["donors_ranked"])
+        assert r["m"] == exp["m"]
+        np.testing.assert_array_equal(r["s1"], exp["s1"])
+        s = r["s1"]
+    np.testing.assert_array_equal(s, fx["s0"])
+
+
+def check_repair_invariants(b, s0, tau, n_sink, n_recent, r):
+    """Properties every repair result must have (Sec. 3.4), independent of how it is computed."""
+    b = np.asarray(b, dtype=np.float64)
+    s0 = np.asarray(s0).astype(bool)
+    s1 = np.asarray(r["s1"]).astype(bool)
+    n = len(b)
+    idx = np.arange(n)
+    prot = (idx < n_sink) | (idx >= n - n_recent)
+    orphan = ~s0 & (b < tau)
+    donor = s0 & ~prot & (b >= tau)
+    m = min(int(orphan.sum()), int(donor.sum()))
+    assert s1.sum() == s0.sum(), "budget changed"
+    admitted, evicted = s1 & ~s0, s0 & ~s1
+    assert admitted.sum() == m and evicted.sum() == m, "swap count is not min(|O|,|D|)"
+    assert not (admitted & ~orphan).any(), "admitted a non-orphan"
+    assert not (evicted & ~donor).any(), "evicted a non-donor"
+    assert not (s0 & prot & ~s1).any(), "evicted a protected token"
+    # severity: every admitted orphan ranks before every orphan left out (b asc, index asc)
+    key_o = lambda i: (b[i], i)
+    key_d = lambda i: (-b[i], i)
+    out_o = idx[orphan & ~admitted]
+    out_d = idx[donor & ~evicted]
+    if m and len(out_o):
+        assert max(map(key_o, idx[admitted])) < min(map(key_o, out_o)), "orphan severity order"
+    if m and len(out_d):
+        assert max(map(key_d, idx[evicted])) < min(map(key_d, out_d)), "donor severity order"
+    assert r["m"] == m and r["n_orphan"] == int(orphan.sum()) and r["n_donor"] == int(donor.sum())
+
+
+def pin_repair_invariants(o):
+    g = np.random.Generator(np.random.PCG64(11))
+    for t in range(300):
+        n = int(g.integers(1, 60))
+        # quantised scores create many exact ties, including values equal to tau
+        b = np.round(g.uniform(-1.0, 1.0, n) * 8) / 8
+        b[g.random(n) < 0.1] = -1.0
+        s0 = (g.random(n) < g.uniform(0.1, 0.9)).astype(np.uint8)
+        tau = float(np.round(g.uniform(-0.5, 1.0) * 8) / 8)
+        n_sink, n_recent = int(g.integers(0, 4)), int(g.integers(0, 4))
+        r = o.repair(b, s0, tau, n_sink, n_recent)
+        check_repair_invariants(b, s0, tau, n_sink, n_recent, r)
+
+
+def pin_exact_noops(o):
+    """tau above every cosine -> no donors; tau below every b (b >= -1) -> no orphans."""
+    g = np.random.Generator(np.random.PCG64(3))
+    for t in range(20):
+        n = int(g.integers(8, 80))
+        K = g.standard_normal((n, 8)).astype(np.float32)
+        K[n // 2] = K[1]
+        s0 = (g.random(n) < 0.5).astype(np.uint8)
+        for tau in (1.5, -1.5):
+            r = o.repair_problem(K, "f32", s0, int(s0.sum()), tau, 2, 1, 1)
+            np.testing.assert_array_equal(r["s1"], s0)
+            assert r["m"] == 0
+            if tau > 1:
+                assert r["n_donor"] == 0
+            else:
+                assert r["n_orphan"] == 0
+
+
+def pin_redundancy_consistent_noop(o):
+    """The paper's no-op check (Sec. 3.4, Sec. 4.1): when every evicted token has a retained
+    twin and no retained token has a retained twin, both sets are empty and S1 = S0."""
+    g = np.random.Generator(np.random.PCG64(5))
+    for t in range(100):
+        n = int(g.integers(6, 48))
+        w = int(g.integers(0, 4))
+        s0 = (g.random(n) < 0.5).astype(np.uint8)
+        s0[0] = 1
+        ret = np.flatnonzero(s0)
+        d = len(ret) + 1
+        K = np.zeros((n, d), np.float32)
+        K[ret, np.arange(len(ret))] = 1.0            # retained keys: mutually orthogonal
+        ok = True
+        for i in np.flatnonzero(s0 == 0):            # evicted: copy of a retained key beyond w
+            far = ret[np.abs(ret - i) > w]
+            if len(far) == 0:
+                ok = False
+                break
+            K[i] = K[far[g.integers(len(far))]]
+        if not ok:
+            continue
+        for tau in (0.85, 0.9, 1.0):
+            r = o.repair_problem(K, "f32", s0, int(s0.sum()), tau, w, 0, 0)
+            assert r["n_orphan"] == 0 and r["n_donor"] == 0
+            np.testing.assert_array_equal(r["s1"], s0)
+
+
+def pin_second_pass_condition(o):
+    """If |D| <= |O| and no two admitted orphans are twins of each other (sim >= tau beyond w),
+    a second pass finds no donors and leaves S1 unchanged.  Proof: a retained non-donor j cannot
+    gain an admitted orphan o as a twin, because sim(j, o) >= tau with j in S0 and |j-o| > w
+    would have given o a surviving twin; and an admitted orphan's best retained similarity is
+    below tau by the condition.  The check runs on random small caches with planted twins."""
+    g = np.random.Generator(np.random.PCG64(13))
+    hits = 0
+    for t in range(150):
+        n = int(g.integers(10, 64))
+        d = 8
+        w = int(g.integers(0, 3))
+        K = g.standard_normal((n, d))
+        for _ in range(n // 3):
+            a, b_ = g.integers(0, n, size=2)
+            K[a] = K[b_] + 0.05 * g.standard_normal(d)
+        K = K.astype(np.float32)
+        s0 = (g.random(n) < 0.5).astype(np.uint8)
+        tau = 0.9
+        r1 = o.repair_problem(K, "f32", s0, int(s0.sum()), tau, w, 1, 1)
+        if not (r1["n_donor"] <= r1["n_orphan"]):
+            continue
+        adm = np.flatnonzero(r1["s1"].astype(bool) & ~s0.astype(bool))
+        Kd = K.astype(np.float64)
+        nrm = np.linalg.norm(Kd, axis=1)
+        twins = False
+        for x in range(len(adm)):
+            for y in range(x + 1, len(adm)):
+                i, j = adm[x], adm[y]
+                if abs(i - j) > w and Kd[i] @ Kd[j] / (nrm[i] * nrm[j]) >= tau:
+                    twins = True
+        if twins:
+            continue
+        r2 = o.repair_problem(K, "f32", r1["s1"], int(s0.sum()), tau, w, 1, 1)
+        assert r2["n_donor"] == 0, "second pass found donors although the condition holds"
+        np.testing.assert_array_equal(r2["s1"], r1["s1"])
+        hits += 1
+    assert hits >= 20, hits
+
+
+def pin_budget_checked(o):
+    K = np.eye(6, dtype=np.float32)
+    s0 = np.array([1, 1, 0, 0, 1, 0], np.uint8)
+    try:
+        o.repair_problem(K, "f32", s0, 2, 0.9, 0, 0, 0)
+    except ValueError:
+        return
+    raise AssertionError("budget != |S0| was accepted")
+
+
+ALL_PINS = [
+    pin_closed_forms, pin_window_and_sentinel, pin_scale_invariance, pin_bf16_decode,
+    pin_nonfinite_rejected, pin_repair_ranked, pin_oscillation, pin_repair_invariants,
+    pin_exact_noops, pin_redundancy_consistent_noop, pin_second_pass_condition,
+    pin_budget_checked,
+]
