@@ -1,0 +1,176 @@
+#!/usr/bin/env python3
+"""Throughput of the TwinKV hot path on one MI355X.
+
+One step = one full repair pass (``twinkv_repair``) over a whole synthetic KV cache already
+resident in HBM: inverse norms and the [S0 | evicted] partition, the fused similarity
+contraction with both masked row max/argmax reductions (all keys and retained keys), then
+orphan / donor classification, severity selection and the budget-preserving swap.
+
+Default workload: the long anisotropic cache, 36 layers x 8 KV heads x 32768 tokens x d=128
+bf16 (288 problems), tau 0.9, w 32, budget floor(0.3 N) + 4 sinks + 128 recent.
+
+Printed: one JSON line with key-pair similarities per second (N^2 ordered pairs per problem
+per step) as ``value``, ms per step (= repair ms per cache), the similarity kernel's roofline
+position (its duration measured live with HIP events on the launch stream) and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(batch, target_s: float = 12.0) -> dict:
+    """The fp64 oracle on a bounded row sample of problem (head 0, sequence 0)."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        cores = os.cpu_count() or 1
+    a, e = int(batch.cu_seqlens[0]), int(batch.cu_seqlens[1])
+    keys, ret = batch.keys[0, a:e], batch.retained[0, a:e]
+    n = e - a
+    w = batch.spec.w
+    probe = min(n, 64)
+    t = time.perf_counter()
+    oracle.nn_scores(keys, batch.dtype, ret, w, rows=np.arange(probe))
+    tp = max(time.perf_counter() - t, 1e-3)
+    rows = int(min(n, max(probe, probe * target_s / tp)))
+    t = time.perf_counter()
+    oracle.nn_scores(keys, batch.dtype, ret, w, rows=np.arange(rows))
+    dt = time.perf_counter() - t
+    return {"value": rows * n / dt, "unit": "pairs/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"oracle.nn_scores (both reductions, fp64) on rows 0..{rows - 1} of "
+                      f"problem (head 0, seq 0), N={n}, d={batch.d}: {rows * n:.3e} ordered pairs "
+                      f"in {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="long_aniso_32k",
+                    help="tiny | llama1b_8k | qwen4b_16k | long_aniso_32k | ragged_64x")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE {world}); problems are independent, so more GPUs would each run the "
+              f"same single-GPU path on their share of heads.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    from paper_2608_27128_amd import binding, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    binding.lib()                                     # fail loudly if the HIP library is missing
+
+    sp = synth.spec(args.workload)
+    t0 = time.perf_counter()
+    batch = synth.make_batch(sp, threads=min(16, os.cpu_count() or 1))
+    log(f"[bench] generated {sp.name}: keys {batch.keys.shape} {batch.dtype} in "
+        f"{time.perf_counter() - t0:.1f} s")
+
+    if batch.dtype == "bf16":
+        keys = torch.from_numpy(batch.keys.view(np.int16)).view(torch.bfloat16).to(dev)
+    else:
+        keys = torch.from_numpy(batch.keys).to(dev)
+    ret = torch.from_numpy(batch.retained).to(dev)
+    cu = batch.cu_seqlens
+    lens = np.diff(cu).astype(np.float64)
+    pairs = float(sp.n_heads * np.sum(lens * lens))      # ordered key pairs per step
+    flops = 2.0 * batch.d * pairs                         # dense masked K K^T, per launch
+
+    def step(outputs=None, ws=None):
+        return binding.repair(keys, ret, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent, cu,
+                              outputs=outputs, workspace=ws)
+
+    out = step()
+    H, T = batch.retained.shape
+    ws = torch.empty((binding.workspace_bytes(binding.OP_REPAIR, 0 if batch.dtype == "bf16" else 1,
+                                              batch.d, H, cu),), dtype=torch.uint8, device=dev)
+    for _ in range(args.warmup):
+        step(out, ws)
+    torch.cuda.synchronize()
+
+    k2_start = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    k2_stop = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    st_start = torch.cuda.Event(enable_timing=True)
+    st_stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    st_start.record()
+    for k in range(args.steps):
+        binding.profile_sim_events(k2_start[k], k2_stop[k])
+        step(out, ws)
+    st_stop.record()
+    binding.profile_sim_events(None, None)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_per_step = 1000.0 * wall / args.steps
+    ev_ms = st_start.elapsed_time(st_stop) / args.steps
+    k2_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(k2_start, k2_stop)]))
+    stats = out["stats"].cpu().numpy()
+    assert (stats[:, 3] == 0).all(), "a problem reported a non-OK status"
+    s1_sum = out["s1"].sum(dim=1).cpu().numpy()
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (events {ev_ms:.3f}); "
+        f"similarity kernel {k2_ms:.3f} ms; swaps {int(stats[:, 2].sum())}; "
+        f"|S1| per head {int(s1_sum.min())}..{int(s1_sum.max())}")
+
+    achieved = flops / (k2_ms * 1e-3) / 1e12
+    result = {
+        "metric": "key-pair sims/sec (TFLOP/s of masked K.K^T, % bf16 MFMA peak); repair ms/cache",
+        "value": pairs / (ms_per_step * 1e-3),
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if batch.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": sp.name, "problems": int(sp.n_heads * sp.n_seqs),
+                   "layers_x_kv_heads": int(sp.n_heads), "seq_lens": sorted(set(int(x) for x in lens))[:4],
+                   "d": int(batch.d), "tau": sp.tau, "w": sp.w, "n_sink": sp.n_sink,
+                   "n_recent": sp.n_recent, "budget": int(batch.budget[0]), "parallelism": "none"},
+        "repair_ms_per_cache": ms_per_step,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "sim_reduce_kernel", "kernel_ms": k2_ms,
+                     "flops_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample ...")
+        result["cpu_baseline"] = cpu_baseline(batch, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,157 @@
+/*
+ * twinkv.h -- C ABI of the TwinKV redundancy / repair library for AMD MI355X (gfx950).
+ *
+ * TwinKV (paper: "TwinKV: A Composable Repair Pass for KV Cache Eviction via Pairwise
+ * Key Redundancy") works per (layer, KV head) on the keys of one sequence (Sec. 3.1):
+ *   - Eq. 1: sim(i, j) = k_hat_i . k_hat_j with k_hat = k / ||k||_2 (Sec. 3.2);
+ *   - twin rule: j is a twin of i iff sim(i, j) > tau and |i - j| > w (Sec. 3.2, Eq. 2);
+ *   - Eq. 4: b_i(S0) = max over j in S0, |i - j| > w of sim(i, j), or -1 if no such j;
+ *   - repair (Sec. 3.4): orphans (i not in S0, b_i < tau) and redundant donors (j in S0,
+ *     outside the protected sink / recent regions, b_j >= tau) are ranked by severity
+ *     (orphans by ascending b, donors by descending b) and the m = min(|O|, |D|) most severe
+ *     pairs are swapped, so |S1| = |S0| = K exactly.
+ *
+ * Problems.  A batch holds n_heads (layer, KV head) pairs times n_seqs sequences.  Sequence s
+ * owns global token positions [cu_seqlens[s], cu_seqlens[s+1]) and T = cu_seqlens[n_seqs].
+ * Problem q = h * n_seqs + s is (head h, sequence s); problems are independent (Sec. 3.1).
+ * Indices reported by the library are 0-based positions inside the sequence.
+ *
+ * Memory.  Unless marked "(host)", pointers are DEVICE pointers owned by the caller.  The
+ * library allocates nothing: scratch space is the caller's `workspace` (size from
+ * twinkv_workspace_bytes).  Keys: element (h, t, c) is at keys[h*head_stride + t*token_stride
+ * + c] (strides in elements, channels contiguous); the pointer and both strides (in bytes)
+ * must be multiples of 16.  Per-token arrays (retained masks, scores, indices) are contiguous
+ * [n_heads][T].  Every entry point enqueues work on `stream` (a hipStream_t passed as void*;
+ * NULL = the default stream) and returns without waiting; results are valid once the stream
+ * has reached that point.  The small per-sequence table built from the host arrays is copied
+ * into the workspace with an asynchronous host-to-device copy from pageable memory, which
+ * consumes the host data before returning.
+ *
+ * Errors.  Argument errors are detected on the host before anything is enqueued and are
+ * returned synchronously (TWINKV_E_*).  A HIP failure while enqueueing returns TWINKV_E_HIP.
+ * Data-dependent conditions are reported per problem (TWINKV_PROBLEM_*), never by failing.
+ * Concurrent calls are safe as long as they use different workspaces.
+ */
+#ifndef TWINKV_H
+#define TWINKV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define TWINKV_OK             0
+#define TWINKV_E_NULL         1  /* a required pointer is NULL */
+#define TWINKV_E_ARG          2  /* an argument value is out of range or inconsistent */
+#define TWINKV_E_UNSUPPORTED  3  /* head dimension or dtype not supported */
+#define TWINKV_E_WORKSPACE    4  /* workspace missing or smaller than required */
+#define TWINKV_E_HIP          5  /* the HIP runtime reported an error */
+
+/* Key element types. */
+#define TWINKV_BF16 0
+#define TWINKV_F32  1
+
+/* Operations, for twinkv_workspace_bytes. */
+#define TWINKV_OP_NN_SCORES          0
+#define TWINKV_OP_REPAIR             1
+#define TWINKV_OP_REPAIR_FROM_SCORES 2
+
+/* Per-problem status codes (stats[q][3] / status[q]). */
+#define TWINKV_PROBLEM_OK              0
+#define TWINKV_PROBLEM_BUDGET_MISMATCH 1  /* |S0| differs from the budget; S1 = S0 */
+#define TWINKV_PROBLEM_NONFINITE       2  /* a key (or a given score) is NaN/Inf; S1 = S0 */
+
+/*
+ * Bytes of workspace `op` needs for this batch; negative (-TWINKV_E_*) on invalid arguments.
+ * cu_seqlens (host, n_seqs + 1 entries, non-decreasing, cu_seqlens[0] = 0).
+ * dtype and d are ignored for TWINKV_OP_REPAIR_FROM_SCORES.
+ */
+int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs,
+                               const int64_t* cu_seqlens);
+
+/*
+ * Best twin of every token (Sec. 3.2 Eq. 1 + the twin rule's window; Sec. 3.4 Eq. 4).
+ *
+ *   keys       [n_heads][T][d] bf16 or fp32 (see Memory).  d must be 64 or 128.
+ *   retained   [n_heads][T] uint8, nonzero = in S0; NULL skips the retained reduction.
+ *   w          window half-width, >= 0: pairs with |i - j| <= w are never compared.
+ *   best_all   [n_heads][T] fp32: max over j with |i-j| > w of sim(i, j); -1 if none.  Nullable.
+ *   arg_all    [n_heads][T] int32: the maximising j (position in the sequence); -1 if none.
+ *              On near-equal candidates the reported j is one whose similarity is within
+ *              1e-5 of the maximum; on exact equality it is the smallest such j.  Nullable.
+ *   best_ret   [n_heads][T] fp32: b_i(S0) of Eq. 4 (-1 if no retained j beyond the window).
+ *              Nullable; must be NULL when retained is NULL.
+ *   arg_ret    [n_heads][T] int32: the maximising retained j, -1 if none.  Nullable.
+ *   status     [n_heads * n_seqs] int32 TWINKV_PROBLEM_* (only OK / NONFINITE).  Nullable.
+ *
+ * Similarities are computed from the stored key values with fp32 accumulation; their error
+ * against exact arithmetic is below 1e-4 for bf16 and fp32 keys.
+ */
+int twinkv_nn_scores(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                     const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                     const uint8_t* retained, int w,
+                     float* best_all, int32_t* arg_all, float* best_ret, int32_t* arg_ret,
+                     int32_t* status,
+                     void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * The full repair pass of Sec. 3.4 for every problem: Eq. 4 scores, orphan / donor
+ * classification, severity ranking and the budget-preserving swap.
+ *
+ *   retained_in   [n_heads][T] uint8, the wrapped policy's S0 (nonzero = retained).
+ *   retained_out  [n_heads][T] uint8, receives S1 as 0/1.  May alias retained_in.
+ *   budget        (host) [n_seqs] int64: K = |S0| of every problem of sequence s.  A problem
+ *                 whose |S0| differs gets TWINKV_PROBLEM_BUDGET_MISMATCH and S1 = S0.
+ *   tau           duplicate threshold (finite).  Orphan: b < tau.  Donor: b >= tau.
+ *   w             window half-width, >= 0.
+ *   n_sink, n_recent  >= 0: positions [0, n_sink) and [len - n_recent, len) are protected
+ *                 (never donors).
+ *   stats         [n_heads * n_seqs][4] int32 = {|O|, |D|, m, status}.
+ *   best_all, arg_all, best_ret, arg_ret   optional outputs as in twinkv_nn_scores (nullable).
+ *                 When best_all and arg_all are both NULL, similarities against evicted keys
+ *                 are skipped (only S0 columns are needed for b).
+ *
+ * Ranking ties resolve by ascending position (among equal b, the earlier orphan is admitted
+ * and the earlier donor evicted first).
+ */
+int twinkv_repair(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                  const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                  const uint8_t* retained_in, uint8_t* retained_out,
+                  const int64_t* budget, float tau, int w, int n_sink, int n_recent,
+                  int32_t* stats,
+                  float* best_all, int32_t* arg_all, float* best_ret, int32_t* arg_ret,
+                  void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * Classification, severity ranking and swap of Sec. 3.4 from given scores b = b_i(S0)
+ * ([n_heads][T] fp32), e.g. produced by twinkv_nn_scores or by another scorer.  Arguments as
+ * in twinkv_repair.  A NaN/Inf score gives TWINKV_PROBLEM_NONFINITE and S1 = S0.
+ */
+int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_t* retained_out,
+                              int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                              const int64_t* budget, float tau, int n_sink, int n_recent,
+                              int32_t* stats,
+                              void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * Profiling hook.  For calls made afterwards from the calling thread, record the given
+ * hipEvent_t handles on the call's stream immediately before and immediately after the
+ * launch of the similarity kernel (the fused contraction + reductions), so its duration can
+ * be read with hipEventElapsedTime.  The events stay owned by the caller; pass NULL, NULL to
+ * stop recording.
+ */
+void twinkv_profile_sim_events(void* start_event, void* stop_event);
+
+/* Static description of a return code (TWINKV_OK, TWINKV_E_*); never freed. */
+const char* twinkv_status_string(int status);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+int twinkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TWINKV_H */

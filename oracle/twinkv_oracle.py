@@ -104,10 +104,8 @@ def best_twin(S: np.ndarray, valid: np.ndarray):
     any_valid = valid.any(axis=1)
     arg = np.argmax(M, axis=1)                     # first maximal index = smallest j
     best = M[np.arange(n_rows), arg]
-    if n >= 2:
-        second = np.partition(M, n - 2, axis=1)[:, n - 2]
-    else:
-        second = np.full(n_rows, -np.inf)
+    M[np.arange(n_rows), arg] = -np.inf            # the runner-up: best of the remaining entries
+    second = M.max(axis=1) if n >= 2 else np.full(n_rows, -np.inf)
     best = np.where(any_valid, best, -1.0)
     arg = np.where(any_valid, arg, -1).astype(np.int64)
     return best, arg, second

@@ -1,0 +1,342 @@
+// Host layer of the C ABI declared in include/twinkv.h: argument validation (pure host code,
+// done before anything is enqueued), workspace layout, the per-sequence schedule table and
+// the kernel launches (K1a normalise, K1b partition, K2 similarity, K3 repair).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <numeric>
+#include <vector>
+
+#include "twinkv.h"
+#include "twinkv_internal.h"
+
+namespace twinkv {
+namespace {
+
+constexpr int kVersion = 100;  // 0.1.0
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Batch {
+  int n_heads = 0, n_seqs = 0;
+  int64_t T = 0, PT = 0;
+};
+
+// Shared checks of the batch description; fills `bt`.
+int check_batch(int n_heads, int n_seqs, const int64_t* cu, Batch& bt) {
+  if (cu == nullptr) return TWINKV_E_NULL;
+  if (n_heads < 1 || n_seqs < 1) return TWINKV_E_ARG;
+  if (cu[0] != 0) return TWINKV_E_ARG;
+  for (int s = 0; s < n_seqs; ++s) {
+    if (cu[s + 1] < cu[s]) return TWINKV_E_ARG;
+  }
+  const int64_t T = cu[n_seqs];
+  const int64_t PT = T + (int64_t)kPermPad * n_seqs;
+  // positions and per-head offsets are 32-bit inside the kernels
+  if (PT > (int64_t)INT32_MAX / 2) return TWINKV_E_ARG;
+  if ((int64_t)n_heads * n_seqs > (int64_t)INT32_MAX / 4) return TWINKV_E_ARG;
+  bt.n_heads = n_heads;
+  bt.n_seqs = n_seqs;
+  bt.T = T;
+  bt.PT = PT;
+  return TWINKV_OK;
+}
+
+Layout layout_for(int op, int dtype, int d, const Batch& bt) {
+  Layout L;
+  size_t off = 0;
+  L.seqtab = off;
+  off = align_up(off + sizeof(SeqInfo) * (size_t)bt.n_seqs);
+  if (op != TWINKV_OP_REPAIR_FROM_SCORES) {
+    const size_t nt = (size_t)bt.n_heads * (size_t)bt.T;
+    const size_t np = (size_t)bt.n_heads * (size_t)bt.PT;
+    L.rinv = off;
+    off = align_up(off + 4 * nt);
+    L.pcol = off;
+    off = align_up(off + 4 * np);
+    L.rcol = off;
+    off = align_up(off + 4 * np);
+    L.pmeta = off;
+    off = align_up(off + sizeof(ProblemMeta) * (size_t)bt.n_heads * bt.n_seqs);
+    if (dtype == TWINKV_F32) {
+      L.hilo = off;
+      off = align_up(off + 2 * nt * (size_t)(2 * d));
+    }
+    if (op == TWINKV_OP_REPAIR) {
+      L.bbuf = off;
+      off = align_up(off + 4 * nt);
+    }
+  }
+  L.total = off + kAlign;  // slack for aligning the caller's base pointer
+  return L;
+}
+
+char* aligned_base(void* ws) {
+  const uintptr_t p = reinterpret_cast<uintptr_t>(ws);
+  return reinterpret_cast<char*>((p + kAlign - 1) / kAlign * kAlign);
+}
+
+int check_keys(const void* keys, int dtype, int d, int64_t head_stride, int64_t token_stride,
+               int w) {
+  if (dtype != TWINKV_BF16 && dtype != TWINKV_F32) return TWINKV_E_UNSUPPORTED;
+  if (d != 64 && d != 128) return TWINKV_E_UNSUPPORTED;
+  if (keys == nullptr) return TWINKV_E_NULL;
+  const int64_t esz = dtype == TWINKV_F32 ? 4 : 2;
+  if (token_stride < d || head_stride < 0) return TWINKV_E_ARG;
+  if ((reinterpret_cast<uintptr_t>(keys) % 16) != 0) return TWINKV_E_ARG;
+  if ((token_stride * esz) % 16 != 0 || (head_stride * esz) % 16 != 0) return TWINKV_E_ARG;
+  if (w < 0) return TWINKV_E_ARG;
+  return TWINKV_OK;
+}
+
+// Builds the per-sequence table (schedule of similarity row blocks, longest first).
+std::vector<SeqInfo> seq_table(const int64_t* cu, int n_seqs, const int64_t* budget, int rows_per_block,
+                               int& total_tiles) {
+  std::vector<SeqInfo> tab(n_seqs);
+  for (int s = 0; s < n_seqs; ++s) {
+    tab[s].start = (int32_t)cu[s];
+    tab[s].len = (int32_t)(cu[s + 1] - cu[s]);
+    tab[s].budget = budget ? (int32_t)budget[s] : -1;
+    tab[s].perm_off = (int32_t)(cu[s] + (int64_t)kPermPad * s);
+  }
+  std::vector<int> order(n_seqs);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int x, int y) { return tab[x].len > tab[y].len; });
+  int cum = 0;
+  for (int r = 0; r < n_seqs; ++r) {
+    const int s = order[r];
+    const int nb = rows_per_block > 0 ? (tab[s].len + rows_per_block - 1) / rows_per_block : 0;
+    tab[r].sorted_seq = s;
+    tab[r].tile_cum = cum;
+    tab[r].nb = nb;
+    tab[r].pad = 0;
+    cum += nb;
+  }
+  total_tiles = cum;
+  return tab;
+}
+
+int hip_status(int e) { return e == 0 ? TWINKV_OK : TWINKV_E_HIP; }
+
+// Events recorded around the similarity kernel (twinkv_profile_sim_events), per thread.
+thread_local hipEvent_t g_sim_start = nullptr;
+thread_local hipEvent_t g_sim_stop = nullptr;
+
+// K1a + K1b + K2 (shared by nn_scores and repair).
+int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_t* cu,
+               const int64_t* budget, int64_t head_stride, int64_t token_stride,
+               const uint8_t* retained, int w, float* best_all, int32_t* arg_all,
+               float* best_ret, int32_t* arg_ret, int32_t* status, char* ws, const Layout& L,
+               bool want_all, void* stream, SeqInfo** seqtab_dev) {
+  int total_tiles = 0;
+  const int rpb = sim_rows_per_block(dtype, d);
+  std::vector<SeqInfo> tab = seq_table(cu, bt.n_seqs, budget, rpb, total_tiles);
+  const int64_t groups = bt.n_heads >= 8 ? 8LL * ((bt.n_heads + 7) / 8) : bt.n_heads;
+  if (groups * total_tiles > (int64_t)INT32_MAX) return TWINKV_E_ARG;
+
+  SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
+  *seqtab_dev = dtab;
+  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
+                     (hipStream_t)stream) != hipSuccess)
+    return TWINKV_E_HIP;
+
+  float* rinv = reinterpret_cast<float*>(ws + L.rinv);
+  int32_t* pcol = reinterpret_cast<int32_t*>(ws + L.pcol);
+  float* rcol = reinterpret_cast<float*>(ws + L.rcol);
+  ProblemMeta* pmeta = reinterpret_cast<ProblemMeta*>(ws + L.pmeta);
+  uint16_t* hilo = dtype == TWINKV_F32 ? reinterpret_cast<uint16_t*>(ws + L.hilo) : nullptr;
+
+  int e = launch_normalise(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, rinv, hilo, stream);
+  if (e) return hip_status(e);
+  e = launch_partition(retained, rinv, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT, pcol, rcol, pmeta,
+                       status, stream);
+  if (e) return hip_status(e);
+
+  SimArgs a;
+  if (dtype == TWINKV_F32) {
+    a.keys = hilo;
+    a.head_stride = bt.T * 2 * d;
+    a.token_stride = 2 * d;
+  } else {
+    a.keys = keys;
+    a.head_stride = head_stride;
+    a.token_stride = token_stride;
+  }
+  a.rinv = rinv;
+  a.pcol = pcol;
+  a.rcol = rcol;
+  a.pmeta = pmeta;
+  a.seqtab = dtab;
+  a.n_heads = bt.n_heads;
+  a.n_seqs = bt.n_seqs;
+  a.T = bt.T;
+  a.PT = bt.PT;
+  // |i - j| <= T - 1 inside any sequence, so any w >= T behaves like w = T.
+  a.w = (int)std::min<int64_t>(w, std::max<int64_t>(bt.T, 1));
+  a.want_all = want_all ? 1 : 0;
+  a.total_tiles = total_tiles;
+  a.best_all = best_all;
+  a.arg_all = arg_all;
+  a.best_ret = best_ret;
+  a.arg_ret = arg_ret;
+  if (g_sim_start && hipEventRecord(g_sim_start, (hipStream_t)stream) != hipSuccess) return TWINKV_E_HIP;
+  e = launch_sim_reduce(a, dtype, d, stream);
+  if (e) return hip_status(e);
+  if (g_sim_stop && hipEventRecord(g_sim_stop, (hipStream_t)stream) != hipSuccess) return TWINKV_E_HIP;
+  return TWINKV_OK;
+}
+
+}  // namespace
+}  // namespace twinkv
+
+using namespace twinkv;
+
+extern "C" {
+
+int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs,
+                               const int64_t* cu_seqlens) {
+  if (op != TWINKV_OP_NN_SCORES && op != TWINKV_OP_REPAIR && op != TWINKV_OP_REPAIR_FROM_SCORES)
+    return -TWINKV_E_ARG;
+  if (op != TWINKV_OP_REPAIR_FROM_SCORES) {
+    if (dtype != TWINKV_BF16 && dtype != TWINKV_F32) return -TWINKV_E_UNSUPPORTED;
+    if (d != 64 && d != 128) return -TWINKV_E_UNSUPPORTED;
+  }
+  Batch bt;
+  const int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return -rc;
+  return (int64_t)layout_for(op, dtype, d, bt).total;
+}
+
+int twinkv_nn_scores(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                     const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                     const uint8_t* retained, int w, float* best_all, int32_t* arg_all,
+                     float* best_ret, int32_t* arg_ret, int32_t* status, void* workspace,
+                     int64_t workspace_bytes, void* stream) {
+  int rc = check_keys(keys, dtype, d, head_stride, token_stride, w);
+  if (rc != TWINKV_OK) return rc;
+  Batch bt;
+  rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  if (retained == nullptr && (best_ret != nullptr || arg_ret != nullptr)) return TWINKV_E_ARG;
+  const Layout L = layout_for(TWINKV_OP_NN_SCORES, dtype, d, bt);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+  SeqInfo* dtab = nullptr;
+  return run_scores(keys, dtype, d, bt, cu_seqlens, nullptr, head_stride, token_stride, retained,
+                    w, best_all, arg_all, best_ret, arg_ret, status, ws, L,
+                    /*want_all=*/true, stream, &dtab);
+}
+
+static int check_repair_common(const uint8_t* retained_in, uint8_t* retained_out,
+                               const int64_t* budget, const int64_t* cu, int n_seqs, float tau,
+                               int n_sink, int n_recent, int32_t* stats) {
+  if (retained_in == nullptr || retained_out == nullptr || budget == nullptr || stats == nullptr)
+    return TWINKV_E_NULL;
+  if (!std::isfinite(tau)) return TWINKV_E_ARG;
+  if (n_sink < 0 || n_recent < 0) return TWINKV_E_ARG;
+  for (int s = 0; s < n_seqs; ++s) {
+    if (budget[s] < 0 || budget[s] > cu[s + 1] - cu[s]) return TWINKV_E_ARG;
+  }
+  return TWINKV_OK;
+}
+
+int twinkv_repair(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                  const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                  const uint8_t* retained_in, uint8_t* retained_out, const int64_t* budget,
+                  float tau, int w, int n_sink, int n_recent, int32_t* stats, float* best_all,
+                  int32_t* arg_all, float* best_ret, int32_t* arg_ret, void* workspace,
+                  int64_t workspace_bytes, void* stream) {
+  int rc = check_keys(keys, dtype, d, head_stride, token_stride, w);
+  if (rc != TWINKV_OK) return rc;
+  Batch bt;
+  rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  rc = check_repair_common(retained_in, retained_out, budget, cu_seqlens, n_seqs, tau, n_sink,
+                           n_recent, stats);
+  if (rc != TWINKV_OK) return rc;
+  const Layout L = layout_for(TWINKV_OP_REPAIR, dtype, d, bt);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+  float* b = best_ret ? best_ret : reinterpret_cast<float*>(ws + L.bbuf);
+  const bool want_all = best_all != nullptr || arg_all != nullptr;
+  SeqInfo* dtab = nullptr;
+  rc = run_scores(keys, dtype, d, bt, cu_seqlens, budget, head_stride, token_stride, retained_in,
+                  w, best_all, arg_all, b, arg_ret, nullptr, ws, L, want_all, stream, &dtab);
+  if (rc != TWINKV_OK) return rc;
+  RepairArgs ra;
+  ra.b = b;
+  ra.s0 = retained_in;
+  ra.s1 = retained_out;
+  ra.seqtab = dtab;
+  ra.pmeta = reinterpret_cast<const ProblemMeta*>(ws + L.pmeta);
+  ra.n_heads = n_heads;
+  ra.n_seqs = n_seqs;
+  ra.T = bt.T;
+  ra.tau = tau;
+  ra.n_sink = n_sink;
+  ra.n_recent = n_recent;
+  ra.stats = stats;
+  return hip_status(launch_repair(ra, stream));
+}
+
+int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_t* retained_out,
+                              int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                              const int64_t* budget, float tau, int n_sink, int n_recent,
+                              int32_t* stats, void* workspace, int64_t workspace_bytes,
+                              void* stream) {
+  if (b == nullptr) return TWINKV_E_NULL;
+  Batch bt;
+  int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  rc = check_repair_common(retained_in, retained_out, budget, cu_seqlens, n_seqs, tau, n_sink,
+                           n_recent, stats);
+  if (rc != TWINKV_OK) return rc;
+  const Layout L = layout_for(TWINKV_OP_REPAIR_FROM_SCORES, 0, 64, bt);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+  int tiles = 0;
+  std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, budget, 0, tiles);
+  SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
+  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
+                     (hipStream_t)stream) != hipSuccess)
+    return TWINKV_E_HIP;
+  RepairArgs ra;
+  ra.b = b;
+  ra.s0 = retained_in;
+  ra.s1 = retained_out;
+  ra.seqtab = dtab;
+  ra.pmeta = nullptr;
+  ra.n_heads = n_heads;
+  ra.n_seqs = n_seqs;
+  ra.T = bt.T;
+  ra.tau = tau;
+  ra.n_sink = n_sink;
+  ra.n_recent = n_recent;
+  ra.stats = stats;
+  return hip_status(launch_repair(ra, stream));
+}
+
+const char* twinkv_status_string(int status) {
+  switch (status) {
+    case TWINKV_OK: return "ok";
+    case TWINKV_E_NULL: return "a required pointer is NULL";
+    case TWINKV_E_ARG: return "invalid argument";
+    case TWINKV_E_UNSUPPORTED: return "unsupported head dimension or key dtype";
+    case TWINKV_E_WORKSPACE: return "workspace missing or too small";
+    case TWINKV_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int twinkv_version(void) { return kVersion; }
+
+void twinkv_profile_sim_events(void* start_event, void* stop_event) {
+  g_sim_start = reinterpret_cast<hipEvent_t>(start_event);
+  g_sim_stop = reinterpret_cast<hipEvent_t>(stop_event);
+}
+
+}  // extern "C"

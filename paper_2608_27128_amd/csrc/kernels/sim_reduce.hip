@@ -1,0 +1,402 @@
+// K2: fused cosine-similarity contraction with two masked row max / argmax reductions.
+//
+// For every problem (head, sequence) and token i it computes, without materialising the
+// N x N matrix (Sec. 3.2 Eq. 1 and the twin window; Sec. 3.4 Eq. 4):
+//   best over all j with |i-j| > w of sim(i, j)        -> best_all / arg_all
+//   best over j in S0 with |i-j| > w of sim(i, j)      -> best_ret / arg_ret  (= b_i(S0))
+// with sim(i, j) = (k_i . k_j) * r_i * r_j, r = 1 / ||k||.
+//
+// Mapping onto gfx950:
+//  * One workgroup owns RB = NWAVES * NSUB * 32 consecutive rows of one problem; each wave
+//    holds NSUB 32-row blocks of its row keys as MFMA B operands in registers for the whole
+//    sweep (d <= 128 makes this a short-K contraction).
+//  * Column keys stream through LDS in tiles of TN = 32 * CPT columns, double buffered, in
+//    the partitioned order [S0 | evicted] written by K1b, so every 32-column chunk belongs to
+//    exactly one of the two reductions.
+//  * v_mfma_f32_32x32x16_bf16 with A = 32 column keys, B = 32 row keys gives each lane one
+//    row i (lane % 32) and 16 columns: register v holds column 8*(v/4) + 4*(lane/32) + v%4.
+//  * Row keys are pre-scaled by an exact power of two g_i so that ||g_i k_i|| is in (0.5, 1];
+//    x = dot * r_j + 3 then lies in [2, 4), where the fp32 bit pattern is monotone and the
+//    low 4 mantissa bits can carry the register slot: one v_max_u32 reduces value and
+//    argmax together (quantum 2^-18 of the scaled similarity, far below the 1e-3 tolerance).
+//    The chunk index of a lane's running maximum is kept beside it.
+//  * Products of bf16 values are exact in fp32; accumulation is fp32.  fp32 keys use the
+//    split k = hi + lo (bf16 each) and the three products hi.hi + lo.hi + hi.lo, laid out
+//    as a contraction over 3d.
+//  * Pairs inside the window and padding columns only occur in a few chunks per wave; those
+//    take a masked epilogue, all others a 2.6-instruction-per-element epilogue.
+#include <hip/hip_runtime.h>
+
+#include "../twinkv_internal.h"
+
+namespace twinkv {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
+struct Cfg {
+  static constexpr int KSTEPS = SPLIT ? 3 * D / 16 : D / 16;
+  static constexpr int DCOL = SPLIT ? 2 * D : D;      // bf16 elements per column in LDS
+  static constexpr int STRIDE = DCOL + 8;             // +16 bytes against bank conflicts
+  static constexpr int TN = CPT * kChunk;
+  static constexpr int SEGS_PER_COL = DCOL / 8;       // 16-byte pieces per column
+  static constexpr int NT = NWAVES * 64;
+  static constexpr int SEGS = TN * SEGS_PER_COL;
+  static constexpr int SEGS_PER_THREAD = SEGS / NT;
+  static constexpr int RB = NWAVES * NSUB * 32;
+  static constexpr int KEY_BYTES = TN * STRIDE * 2;
+  static constexpr int STAGE = KEY_BYTES + TN * 4 + TN * 4;
+  static_assert(SEGS % NT == 0, "tile copy must divide evenly");
+  static_assert(TN <= NT, "one thread per tile column for the column tables");
+};
+
+// Element offset of k-step t inside a column (A operand) / a row (B operand).
+// bf16 keys: plain. fp32 keys: columns hold [hi | lo], rows hold [hi | lo]; the three
+// k-step groups pair (col hi, row hi), (col lo, row hi), (col hi, row lo).
+template <int D, bool SPLIT>
+__device__ constexpr int col_off(int t) {
+  if constexpr (!SPLIT) {
+    return t * 16;
+  } else {
+    constexpr int G = D / 16;
+    return t < G ? t * 16 : (t < 2 * G ? D + (t - G) * 16 : (t - 2 * G) * 16);
+  }
+}
+template <int D, bool SPLIT>
+__device__ constexpr int row_off(int t) {
+  if constexpr (!SPLIT) {
+    return t * 16;
+  } else {
+    constexpr int G = D / 16;
+    return t < G ? t * 16 : (t < 2 * G ? (t - G) * 16 : D + (t - 2 * G) * 16);
+  }
+}
+
+// Power of two g with ||g k|| in (0.5, 1] given r = 1/||k|| (1 for zero or bad keys).
+__device__ inline float row_scale(float r) {
+  if (!(r > 0.0f) || !(r < 3.0e38f)) return 1.0f;
+  int e;
+  (void)frexpf(r, &e);
+  return ldexpf(1.0f, e - 1);
+}
+
+// Multiply 8 bf16 values by a power of two.  Exact unless a value leaves the normal range.
+__device__ inline bf16x8 scale8(uint4 raw, float g) {
+  uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float lo = __uint_as_float(w[k] << 16) * g;
+    const float hi = __uint_as_float(w[k] & 0xFFFF0000u) * g;
+    o[k] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+  }
+  uint4 r = make_uint4(o[0], o[1], o[2], o[3]);
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+// Column (0..31 inside a chunk) held by register v of a lane in half `half`.
+__device__ inline int slot_col(int v, int half) { return 8 * (v >> 2) + 4 * half + (v & 3); }
+
+constexpr uint32_t kValidMin = 0x3F800000u;  // packed values >= 1.0f are real candidates
+
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
+__global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
+  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT>;
+  __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
+
+  // ---- which (head, sequence, row block) this workgroup owns --------------------------
+  // With >= 8 heads, heads h = x (mod 8) go to the XCD x the hardware dispatches block
+  // b = x (mod 8) to, so one problem's row blocks share that XCD's L2; inside an XCD the
+  // sequences run longest first.
+  int k, hx, h0, hstep;
+  if (a.n_heads >= 8) {
+    const int x = blockIdx.x & 7;
+    k = blockIdx.x >> 3;
+    hx = (a.n_heads - x + 7) >> 3;
+    h0 = x;
+    hstep = 8;
+  } else {
+    k = blockIdx.x;
+    hx = a.n_heads;
+    h0 = 0;
+    hstep = 1;
+  }
+  if (k >= hx * a.total_tiles) return;
+  int lo = 0, hi = a.n_seqs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (hx * a.seqtab[mid].tile_cum <= k) lo = mid; else hi = mid - 1;
+  }
+  const int nb = a.seqtab[lo].nb;
+  const int local = k - hx * a.seqtab[lo].tile_cum;
+  const int head = h0 + hstep * (local / nb);
+  const int rb = local - (local / nb) * nb;
+  const int seq = a.seqtab[lo].sorted_seq;
+  const SeqInfo si = a.seqtab[seq];
+  const int q = head * a.n_seqs + seq;
+  const ProblemMeta pm = a.pmeta[q];
+  const int len = si.len;
+  const int nchunks = a.want_all ? pm.total_chunks : pm.ret_chunks;
+  const int ncols = nchunks * kChunk;
+  const int ntiles = (nchunks + CPT - 1) / CPT;
+
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int half = lane >> 5;
+  const int l32 = lane & 31;
+  const int wrow0 = rb * C::RB + wave * NSUB * 32;
+
+  const uint16_t* kb = (const uint16_t*)a.keys + (int64_t)head * a.head_stride +
+                       (int64_t)si.start * a.token_stride;
+  const int32_t* pc = a.pcol + (int64_t)head * a.PT + si.perm_off;
+  const float* rc = a.rcol + (int64_t)head * a.PT + si.perm_off;
+  const float* rinv = a.rinv + (int64_t)head * a.T + si.start;
+
+  // ---- row keys: MFMA B operands, resident for the whole sweep ------------------------
+  bf16x8 bfrag[NSUB][C::KSTEPS];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    const int i = wrow0 + s * 32 + l32;
+    const bool ok = i < len;
+    const float g = row_scale(ok ? rinv[i] : 0.0f);
+#pragma unroll
+    for (int t = 0; t < C::KSTEPS; ++t) {
+      uint4 raw = make_uint4(0, 0, 0, 0);
+      if (ok) raw = *reinterpret_cast<const uint4*>(kb + (int64_t)i * a.token_stride +
+                                                     row_off<D, SPLIT>(t) + half * 8);
+      bfrag[s][t] = scale8(raw, g);
+    }
+  }
+
+  uint32_t run_r[NSUB], run_e[NSUB];
+  int cid_r[NSUB], cid_e[NSUB];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    run_r[s] = 0u;
+    run_e[s] = 0u;
+    cid_r[s] = 0;
+    cid_e[s] = 0;
+  }
+
+  // ---- column tiles: global -> registers -> LDS, double buffered -----------------------
+  // The column index list is read one tile ahead of the key rows it addresses, so the
+  // dependent key loads of tile t+1 never wait on the index loads.
+  int jseg[C::SEGS_PER_THREAD];       // column of each 16-byte piece, next tile to copy
+  int cur_p = -1, nxt_p = -1;         // column index / inverse norm of this thread's column
+  float cur_r = 0.0f, nxt_r = 0.0f;
+  uint4 pre[C::SEGS_PER_THREAD];
+  auto load_cols = [&](int tile) {
+#pragma unroll
+    for (int e = 0; e < C::SEGS_PER_THREAD; ++e) {
+      const int seg = threadIdx.x + e * C::NT;
+      const int p = tile * C::TN + seg / C::SEGS_PER_COL;
+      jseg[e] = p < ncols ? pc[p] : -1;
+    }
+    if (threadIdx.x < C::TN) {
+      const int p = tile * C::TN + threadIdx.x;
+      nxt_p = p < ncols ? pc[p] : -1;
+      nxt_r = p < ncols ? rc[p] : 0.0f;
+    }
+  };
+  auto load_keys = [&]() {
+#pragma unroll
+    for (int e = 0; e < C::SEGS_PER_THREAD; ++e) {
+      const int seg = threadIdx.x + e * C::NT;
+      const int part = seg - (seg / C::SEGS_PER_COL) * C::SEGS_PER_COL;
+      pre[e] = make_uint4(0, 0, 0, 0);
+      if (jseg[e] >= 0)
+        pre[e] = *reinterpret_cast<const uint4*>(kb + (int64_t)jseg[e] * a.token_stride + part * 8);
+    }
+    cur_p = nxt_p;
+    cur_r = nxt_r;
+  };
+  auto store_tile = [&](int buf) {
+    char* st = smem + buf * C::STAGE;
+    uint16_t* lk = reinterpret_cast<uint16_t*>(st);
+    float* lr = reinterpret_cast<float*>(st + C::KEY_BYTES);
+    int* lp = reinterpret_cast<int*>(st + C::KEY_BYTES + C::TN * 4);
+#pragma unroll
+    for (int e = 0; e < C::SEGS_PER_THREAD; ++e) {
+      const int seg = threadIdx.x + e * C::NT;
+      const int lc = seg / C::SEGS_PER_COL;
+      const int part = seg - lc * C::SEGS_PER_COL;
+      *reinterpret_cast<uint4*>(lk + lc * C::STRIDE + part * 8) = pre[e];
+    }
+    if (threadIdx.x < C::TN) {
+      lr[threadIdx.x] = cur_r;
+      lp[threadIdx.x] = cur_p;
+    }
+  };
+
+  if (ntiles > 0) {
+    load_cols(0);
+    load_keys();
+    store_tile(0);
+    if (ntiles > 1) load_cols(1);
+  }
+  __syncthreads();
+
+  const int band_lo = wrow0 - a.w;                 // columns with j >= band_lo and
+  const int band_hi = wrow0 + NSUB * 32 - 1 + a.w; // j <= band_hi may fall inside a window
+
+  for (int tile = 0; tile < ntiles; ++tile) {
+    if (tile + 1 < ntiles) {
+      load_keys();
+      if (tile + 2 < ntiles) load_cols(tile + 2);
+    }
+    const char* st = smem + (tile & 1) * C::STAGE;
+    const uint16_t* lk = reinterpret_cast<const uint16_t*>(st);
+    const float* lr = reinterpret_cast<const float*>(st + C::KEY_BYTES);
+    const int* lp = reinterpret_cast<const int*>(st + C::KEY_BYTES + C::TN * 4);
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      const int gc = tile * CPT + c;
+      if (gc >= nchunks) break;
+      bf16x8 af[C::KSTEPS];
+      const int col = c * kChunk + l32;
+#pragma unroll
+      for (int t = 0; t < C::KSTEPS; ++t)
+        af[t] = *reinterpret_cast<const bf16x8*>(lk + col * C::STRIDE + col_off<D, SPLIT>(t) + half * 8);
+      float rv[16];
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 x = *reinterpret_cast<const float4*>(lr + c * kChunk + 8 * g4 + 4 * half);
+        rv[4 * g4 + 0] = x.x;
+        rv[4 * g4 + 1] = x.y;
+        rv[4 * g4 + 2] = x.z;
+        rv[4 * g4 + 3] = x.w;
+      }
+      const int first = lp[c * kChunk];
+      const int last = lp[c * kChunk + kChunk - 1];
+      const bool slow = (last < 0) || (first <= band_hi && last >= band_lo);
+      const bool in_ret = gc < pm.ret_chunks;
+      int jv[16];
+      if (slow) {
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int4 x = *reinterpret_cast<const int4*>(lp + c * kChunk + 8 * g4 + 4 * half);
+          jv[4 * g4 + 0] = x.x;
+          jv[4 * g4 + 1] = x.y;
+          jv[4 * g4 + 2] = x.z;
+          jv[4 * g4 + 3] = x.w;
+        }
+      }
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < C::KSTEPS; ++t)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], acc, 0, 0, 0);
+        uint32_t best = 0u;
+        if (!slow) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float x = fmaf(acc[v], rv[v], 3.0f);
+            const uint32_t u = (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
+            best = max(best, u);
+          }
+        } else {
+          const int i = wrow0 + s * 32 + l32;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float x = fmaf(acc[v], rv[v], 3.0f);
+            const uint32_t u = (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
+            const int j = jv[v];
+            const bool ok = (j >= 0) && (abs(i - j) > a.w);
+            best = max(best, ok ? u : 0u);
+          }
+        }
+        // strictly larger value (slot bits ignored): an earlier chunk keeps exact ties
+        if (in_ret) {
+          if ((best >> 4) > (run_r[s] >> 4)) { run_r[s] = best; cid_r[s] = gc; }
+        } else {
+          if ((best >> 4) > (run_e[s] >> 4)) { run_e[s] = best; cid_e[s] = gc; }
+        }
+      }
+    }
+    if (tile + 1 < ntiles) store_tile((tile + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- resolve: lanes l and l+32 hold the same row over disjoint column halves ----------
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    const int i = wrow0 + s * 32 + l32;
+    const float ri = (i < len) ? rinv[i] : 0.0f;
+    const float g = row_scale(ri);
+    uint32_t val[2];
+    int pos[2];
+    const uint32_t runs[2] = {run_r[s], run_e[s]};
+    const int cids[2] = {cid_r[s], cid_e[s]};
+#pragma unroll
+    for (int grp = 0; grp < 2; ++grp) {
+      uint32_t v = runs[grp] & 0xFFFFFFF0u;
+      int p = cids[grp] * kChunk + slot_col(15 - (int)(runs[grp] & 15u), half);
+      const uint32_t v2 = __shfl_xor(v, 32);
+      const int p2 = __shfl_xor(p, 32);
+      if (v2 > v || (v2 == v && p2 < p)) { v = v2; p = p2; }
+      val[grp] = v;
+      pos[grp] = p;
+    }
+    if (half == 0 && i < len) {
+      const int64_t o = (int64_t)head * a.T + si.start + i;
+      const bool vr = val[0] >= kValidMin;
+      const bool ve = val[1] >= kValidMin;
+      const int jr = vr ? pc[pos[0]] : -1;
+      const int je = ve ? pc[pos[1]] : -1;
+      const float sr = vr ? (__uint_as_float(val[0]) - 3.0f) * ri / g : -1.0f;
+      const float se = ve ? (__uint_as_float(val[1]) - 3.0f) * ri / g : -1.0f;
+      if (a.best_ret) a.best_ret[o] = sr;
+      if (a.arg_ret) a.arg_ret[o] = jr;
+      if (a.best_all || a.arg_all) {
+        bool take_r;
+        if (!vr) take_r = false;
+        else if (!ve) take_r = true;
+        else take_r = (val[0] > val[1]) || (val[0] == val[1] && jr < je);
+        const bool any = vr || ve;
+        if (a.best_all) a.best_all[o] = any ? (take_r ? sr : se) : -1.0f;
+        if (a.arg_all) a.arg_all[o] = any ? (take_r ? jr : je) : -1;
+      }
+    }
+  }
+}
+
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
+hipError_t run(const SimArgs& a, hipStream_t st) {
+  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT>;
+  const int64_t groups = a.n_heads >= 8 ? 8LL * ((a.n_heads + 7) / 8) : (int64_t)a.n_heads;
+  const int64_t blocks = groups * a.total_tiles;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT>), dim3((unsigned)blocks),
+                     dim3(C::NT), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Tile shapes: (NSUB 32-row blocks per wave, waves per workgroup, 32-column chunks per tile).
+#define TWINKV_CFG_BF16_128 128, false, 2, 8, 2
+#define TWINKV_CFG_BF16_64 64, false, 4, 8, 2
+#define TWINKV_CFG_F32_64 64, true, 2, 4, 2
+#define TWINKV_CFG_F32_128 128, true, 1, 4, 1
+
+int sim_rows_per_block(int dtype, int d) {
+  if (dtype == 0 && d == 128) return Cfg<TWINKV_CFG_BF16_128>::RB;
+  if (dtype == 0 && d == 64) return Cfg<TWINKV_CFG_BF16_64>::RB;
+  if (dtype == 1 && d == 64) return Cfg<TWINKV_CFG_F32_64>::RB;
+  if (dtype == 1 && d == 128) return Cfg<TWINKV_CFG_F32_128>::RB;
+  return 0;
+}
+
+int launch_sim_reduce(const SimArgs& a, int dtype, int d, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == 0 && d == 128) return run<TWINKV_CFG_BF16_128>(a, st);
+  if (dtype == 0 && d == 64) return run<TWINKV_CFG_BF16_64>(a, st);
+  if (dtype == 1 && d == 64) return run<TWINKV_CFG_F32_64>(a, st);
+  if (dtype == 1 && d == 128) return run<TWINKV_CFG_F32_128>(a, st);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace twinkv

@@ -1,0 +1,97 @@
+// Internal declarations shared by the host layer (api.cpp) and the HIP kernels.
+// Nothing here is part of the public ABI (include/twinkv.h).
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+namespace twinkv {
+
+// Per-sequence table copied into the workspace.  Entries [s].start/len/budget/perm_off
+// describe sequence s; entries [r].sorted_seq/tile_cum/nb describe the sequence of rank r
+// in the longest-first order used to schedule similarity tiles.
+struct SeqInfo {
+  int32_t start;       // first global token of the sequence
+  int32_t len;         // tokens in the sequence
+  int32_t budget;      // |S0| every problem of this sequence must have (-1: not checked)
+  int32_t perm_off;    // offset of this sequence's partitioned column list inside a head
+  int32_t sorted_seq;  // sequence at rank r (longest first)
+  int32_t tile_cum;    // row-block tiles of ranks < r
+  int32_t nb;          // row-block tiles of the sequence at rank r
+  int32_t pad;
+};
+
+// Per-problem result of the partition step.
+struct ProblemMeta {
+  int32_t n_ret;         // |S0|
+  int32_t ret_chunks;    // 32-column chunks holding S0 (last one padded)
+  int32_t total_chunks;  // chunks of S0 followed by chunks of the evicted columns
+  int32_t flags;         // bit 0: a key of the problem is non-finite
+};
+
+constexpr int kChunk = 32;           // columns per MFMA chunk (the 32x32x16 tile)
+constexpr int kPermPad = 2 * kChunk; // padding per (head, sequence) in the column lists
+constexpr int kFlagNonfinite = 1;
+
+// Workspace layout shared by the size query and the launchers.
+struct Layout {
+  size_t seqtab = 0, rinv = 0, pcol = 0, rcol = 0, pmeta = 0, hilo = 0, bbuf = 0;
+  size_t total = 0;
+};
+
+// ---- launchers (defined in the kernel translation units) ----
+// Each returns 0 on success or a hipError_t value.
+
+// K1a: inverse l2 norm of every key (fp64 accumulation) and, for fp32 keys, the bf16
+// hi/lo planes [n_heads][T][2d] the similarity kernel multiplies.
+int launch_normalise(const void* keys, int dtype, int d, int n_heads, int64_t T,
+                     int64_t head_stride, int64_t token_stride, float* rinv, uint16_t* hilo,
+                     void* stream);
+
+// K1b: stable partition of each problem's positions into [S0 | evicted] column lists,
+// padded to whole chunks, with the inverse norm of every listed column.
+int launch_partition(const uint8_t* retained, const float* rinv, const SeqInfo* seqtab,
+                     int n_heads, int n_seqs, int64_t T, int64_t PT, int32_t* pcol, float* rcol,
+                     ProblemMeta* pmeta, int32_t* status, void* stream);
+
+struct SimArgs {
+  const void* keys;          // bf16 keys, or the hi/lo planes for fp32 keys
+  int64_t head_stride;       // elements (of uint16) between heads of `keys`
+  int64_t token_stride;      // elements between tokens of `keys`
+  const float* rinv;         // [n_heads][T]
+  const int32_t* pcol;       // [n_heads][PT]
+  const float* rcol;         // [n_heads][PT]
+  const ProblemMeta* pmeta;  // [n_heads * n_seqs]
+  const SeqInfo* seqtab;     // [n_seqs]
+  int n_heads, n_seqs;
+  int64_t T, PT;
+  int w;
+  int want_all;              // also reduce over evicted columns (best_all / arg_all)
+  int total_tiles;           // row-block tiles of all sequences (sum of nb)
+  float* best_all;
+  int32_t* arg_all;
+  float* best_ret;
+  int32_t* arg_ret;
+};
+
+// Rows covered by one workgroup of the similarity kernel for this (dtype, d).
+int sim_rows_per_block(int dtype, int d);
+// K2: fused MFMA similarity with the two masked row max / argmax reductions.
+int launch_sim_reduce(const SimArgs& a, int dtype, int d, void* stream);
+
+struct RepairArgs {
+  const float* b;            // [n_heads][T]
+  const uint8_t* s0;         // [n_heads][T]
+  uint8_t* s1;               // [n_heads][T]
+  const SeqInfo* seqtab;
+  const ProblemMeta* pmeta;  // nullable: key status from the partition step
+  int n_heads, n_seqs;
+  int64_t T;
+  float tau;
+  int n_sink, n_recent;
+  int32_t* stats;            // [n_heads * n_seqs][4]
+};
+// K3: orphan / donor classification, radix selection of the m most severe, swap.
+int launch_repair(const RepairArgs& a, void* stream);
+
+}  // namespace twinkv

@@ -48,8 +48,9 @@ __all__ = [
 def bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32/float64 values to bf16 (round-to-nearest-even); return raw uint16 bits."""
     f = np.ascontiguousarray(x, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = f.view(np.uint32)
+    # finite inputs stay below 2^32 after adding the rounding increment
+    rounded = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return rounded.astype(np.uint16)
 
 
@@ -224,19 +225,25 @@ def _rng(sp: Spec, s: int, h: int) -> np.random.Generator:
 
 def _base_keys(sp: Spec, g: np.random.Generator, n: int) -> np.ndarray:
     d = sp.d
+    f32 = np.float32
     if sp.key_recipe == "iid":
-        return g.standard_normal((n, d))
+        return g.standard_normal((n, d), dtype=f32)
     if sp.key_recipe == "offset":
-        mu = g.normal(0.0, sp.offset_sd, size=d)
-        return mu[None, :] + g.standard_normal((n, d))
+        mu = g.normal(0.0, sp.offset_sd, size=d).astype(f32)
+        K = g.standard_normal((n, d), dtype=f32)
+        K += mu[None, :]
+        return K
     if sp.key_recipe == "aniso":
-        U = g.standard_normal((d, sp.rank))
-        z = g.standard_normal((n, sp.rank))
+        U = g.standard_normal((d, sp.rank), dtype=f32)
+        z = g.standard_normal((n, sp.rank), dtype=f32)
         chans = g.choice(d, size=sp.n_outliers, replace=False)
         signs = np.where(g.random(sp.n_outliers) < 0.5, -1.0, 1.0)
-        o = np.zeros(d)
+        o = np.zeros(d, dtype=f32)
         o[chans] = signs * sp.outlier_mag
-        return z @ U.T + o[None, :] + g.standard_normal((n, d))
+        K = z @ U.T
+        K += o[None, :]
+        K += g.standard_normal((n, d), dtype=f32)
+        return K
     raise ValueError(f"unknown key recipe {sp.key_recipe!r}")
 
 
@@ -276,7 +283,7 @@ def _plant(sp: Spec, g: np.random.Generator, K: np.ndarray) -> None:
     if sp.dup_recipe == "uniform":
         tgt = np.sort(g.choice(np.arange(1, n), size=min(n_copies, n - 1), replace=False))
         src = np.floor(g.random(len(tgt)) * tgt).astype(np.int64)   # uniform in [0, t)
-        noise = g.normal(0.0, sp.dup_sigma, size=(len(tgt), d))
+        noise = (sp.dup_sigma * g.standard_normal((len(tgt), d), dtype=np.float32))
         _resolve_copies(K, tgt, src, noise)
         return
     if sp.dup_recipe == "clusters":
@@ -300,7 +307,7 @@ def _plant(sp: Spec, g: np.random.Generator, K: np.ndarray) -> None:
             planted += size - 1
         tgt = np.asarray(tg, dtype=np.int64)
         src = np.asarray(sr, dtype=np.int64)
-        noise = g.normal(0.0, sp.dup_sigma, size=(len(tgt), d))
+        noise = (sp.dup_sigma * g.standard_normal((len(tgt), d), dtype=np.float32))
         # sources are never targets here, so a single simultaneous update is exact
         K[tgt] = K[src] + noise
         return
@@ -313,7 +320,7 @@ def _rope(sp: Spec, K: np.ndarray) -> np.ndarray:
     c = np.arange(half, dtype=np.float64)
     theta = sp.rope_base ** (-2.0 * c / d)
     ang = np.arange(n, dtype=np.float64)[:, None] * theta[None, :]
-    cs, sn = np.cos(ang), np.sin(ang)
+    cs, sn = np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32)
     x, y = K[:, :half], K[:, half:]
     return np.concatenate([x * cs - y * sn, x * sn + y * cs], axis=1)
 

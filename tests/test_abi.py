@@ -1,0 +1,129 @@
+"""The C-ABI library loads, exports every symbol include/twinkv.h declares, and rejects bad
+arguments on the host before enqueueing any GPU work (no GPU needed: validation is host code
+and never reaches a HIP call)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_27128_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "twinkv.h")
+
+E_NULL, E_ARG, E_UNSUP, E_WS = 1, 2, 3, 4
+FAKE = 0x100000          # 16-byte aligned stand-in for a device pointer; never dereferenced
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(twinkv_\w+)\s*\(", src)))
+
+
+def test_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 6, names
+    L = binding.lib()
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in twinkv.h but not exported"
+    assert set(names) == set(binding.SIGNATURES), "binding signatures out of sync with the header"
+
+
+def test_version_and_strings():
+    assert binding.version() == 100
+    for code in range(6):
+        assert binding.status_string(code) and "unknown" not in binding.status_string(code)
+    assert "unknown" in binding.status_string(99)
+
+
+def cu_arr(v):
+    return (ctypes.c_int64 * len(v))(*v)
+
+
+def test_workspace_bytes():
+    L = binding.lib()
+    a = L.twinkv_workspace_bytes(0, 0, 128, 8, 1, cu_arr([0, 1000]))
+    b = L.twinkv_workspace_bytes(0, 0, 128, 8, 1, cu_arr([0, 2000]))
+    assert 0 < a < b
+    f32 = L.twinkv_workspace_bytes(0, 1, 64, 8, 1, cu_arr([0, 1000]))
+    bf = L.twinkv_workspace_bytes(0, 0, 64, 8, 1, cu_arr([0, 1000]))
+    assert f32 > bf                       # fp32 keys add the hi/lo planes
+    rep = L.twinkv_workspace_bytes(1, 0, 64, 8, 1, cu_arr([0, 1000]))
+    assert rep > bf                       # repair adds the score buffer
+    assert L.twinkv_workspace_bytes(2, 0, 0, 8, 1, cu_arr([0, 1000])) > 0
+    assert L.twinkv_workspace_bytes(0, 0, 96, 8, 1, cu_arr([0, 10])) == -E_UNSUP
+    assert L.twinkv_workspace_bytes(0, 5, 64, 8, 1, cu_arr([0, 10])) == -E_UNSUP
+    assert L.twinkv_workspace_bytes(7, 0, 64, 8, 1, cu_arr([0, 10])) == -E_ARG
+    assert L.twinkv_workspace_bytes(0, 0, 64, 0, 1, cu_arr([0, 10])) == -E_ARG
+    assert L.twinkv_workspace_bytes(0, 0, 64, 8, 2, cu_arr([0, 10, 5])) == -E_ARG
+    assert L.twinkv_workspace_bytes(0, 0, 64, 8, 1, cu_arr([3, 10])) == -E_ARG
+    assert L.twinkv_workspace_bytes(0, 0, 64, 8, 1, None) == -E_NULL
+
+
+def nn(keys=FAKE, dtype=0, d=64, H=2, cu=(0, 100), hs=6400, ts=64, ret=None, w=32,
+       ba=FAKE, aa=FAKE, br=None, ar=None, st=None, ws=FAKE, wsb=1 << 40):
+    L = binding.lib()
+    return L.twinkv_nn_scores(keys, dtype, d, H, len(cu) - 1, cu_arr(list(cu)), hs, ts, ret, w,
+                              ba, aa, br, ar, st, ws, wsb, None)
+
+
+def test_nn_scores_validation():
+    assert nn(keys=None) == E_NULL
+    assert nn(d=96) == E_UNSUP
+    assert nn(dtype=3) == E_UNSUP
+    assert nn(keys=FAKE + 8) == E_ARG          # misaligned
+    assert nn(ts=60) == E_ARG                  # token stride shorter than d
+    assert nn(ts=68) == E_ARG                  # token stride not a multiple of 16 bytes
+    assert nn(hs=-64) == E_ARG
+    assert nn(w=-1) == E_ARG
+    assert nn(H=0) == E_ARG
+    assert nn(cu=(0, 50, 40)) == E_ARG
+    assert nn(cu=(1, 50)) == E_ARG
+    assert nn(br=FAKE) == E_ARG                # retained reduction without a retained set
+    assert nn(ws=None) == E_WS
+    assert nn(wsb=16) == E_WS
+
+
+def rep(keys=FAKE, dtype=0, d=64, H=2, cu=(0, 100), rin=FAKE, rout=FAKE, budget=(50,), tau=0.9,
+        w=32, ns=4, nr=64, stats=FAKE, ws=FAKE, wsb=1 << 40):
+    L = binding.lib()
+    bud = cu_arr(list(budget)) if budget is not None else None
+    return L.twinkv_repair(keys, dtype, d, H, len(cu) - 1, cu_arr(list(cu)), 6400, 64, rin, rout,
+                           bud, tau, w, ns, nr, stats, None, None, None, None, ws, wsb, None)
+
+
+def test_repair_validation():
+    assert rep(rin=None) == E_NULL
+    assert rep(rout=None) == E_NULL
+    assert rep(stats=None) == E_NULL
+    assert rep(budget=None) == E_NULL
+    assert rep(tau=float("nan")) == E_ARG
+    assert rep(tau=float("inf")) == E_ARG
+    assert rep(budget=(101,)) == E_ARG          # budget larger than the sequence
+    assert rep(budget=(-1,)) == E_ARG
+    assert rep(ns=-1) == E_ARG
+    assert rep(nr=-2) == E_ARG
+    assert rep(d=32) == E_UNSUP
+    assert rep(wsb=100) == E_WS
+
+
+def test_repair_from_scores_validation():
+    L = binding.lib()
+
+    def call(b=FAKE, rin=FAKE, rout=FAKE, budget=(5,), tau=0.9, ns=0, nr=0, stats=FAKE, wsb=1 << 30):
+        return L.twinkv_repair_from_scores(b, rin, rout, 1, 1, cu_arr([0, 10]), cu_arr(list(budget)),
+                                           tau, ns, nr, stats, FAKE, wsb, None)
+    assert call(b=None) == E_NULL
+    assert call(stats=None) == E_NULL
+    assert call(tau=float("nan")) == E_ARG
+    assert call(budget=(11,)) == E_ARG
+    assert call(wsb=0) == E_WS
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError):
+        binding.nn_scores(torch.zeros((4, 64), dtype=torch.bfloat16))
