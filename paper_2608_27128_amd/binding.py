@@ -88,11 +88,18 @@ def workspace_bytes(op: int, dtype: int, d: int, n_heads: int, cu_seqlens) -> in
     return n
 
 
+def _event_handle(e):
+    if e is None:
+        return None
+    if isinstance(e, ctypes.c_void_p):
+        return e.value
+    return int(e)
+
+
 def profile_sim_events(start=None, stop=None) -> None:
-    """Record torch.cuda.Event objects around the similarity kernel of later calls on this
-    thread (None, None stops)."""
-    lib().twinkv_profile_sim_events(None if start is None else start.cuda_event,
-                                    None if stop is None else stop.cuda_event)
+    """Record two hipEvent_t handles (ints or c_void_p) around the similarity kernel of later
+    calls on this thread (None, None stops)."""
+    lib().twinkv_profile_sim_events(_event_handle(start), _event_handle(stop))
 
 
 def _torch():
