@@ -98,6 +98,9 @@ def main() -> int:
                     help="tiny | llama1b_8k | qwen4b_16k | long_aniso_32k | ragged_64x")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first copy this many MiB device-to-device: a dispatch of known size "
+                         "against which memory-traffic counters are scaled")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -117,6 +120,14 @@ def main() -> int:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     binding.lib()                                     # fail loudly if the HIP library is missing
+
+    if args.copy_calibration_mib > 0:
+        src = torch.ones((args.copy_calibration_mib << 20,), dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"[bench] calibration copy of {args.copy_calibration_mib} MiB done")
 
     sp = synth.spec(args.workload)
     t0 = time.perf_counter()

@@ -59,12 +59,17 @@ Layout layout_for(int op, int dtype, int d, const Batch& bt) {
     off = align_up(off + 4 * np);
     L.rcol = off;
     off = align_up(off + 4 * np);
+    L.prank = off;
+    off = align_up(off + 4 * np);
     L.pmeta = off;
     off = align_up(off + sizeof(ProblemMeta) * (size_t)bt.n_heads * bt.n_seqs);
+    const size_t dcol = dtype == TWINKV_F32 ? (size_t)(2 * d) : (size_t)d;
     if (dtype == TWINKV_F32) {
       L.hilo = off;
-      off = align_up(off + 2 * nt * (size_t)(2 * d));
+      off = align_up(off + 2 * nt * dcol);
     }
+    L.pkeys = off;
+    off = align_up(off + 2 * np * dcol);
     if (op == TWINKV_OP_REPAIR) {
       L.bbuf = off;
       off = align_up(off + 4 * nt);
@@ -147,13 +152,15 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
   float* rinv = reinterpret_cast<float*>(ws + L.rinv);
   int32_t* pcol = reinterpret_cast<int32_t*>(ws + L.pcol);
   float* rcol = reinterpret_cast<float*>(ws + L.rcol);
+  int32_t* prank = reinterpret_cast<int32_t*>(ws + L.prank);
   ProblemMeta* pmeta = reinterpret_cast<ProblemMeta*>(ws + L.pmeta);
   uint16_t* hilo = dtype == TWINKV_F32 ? reinterpret_cast<uint16_t*>(ws + L.hilo) : nullptr;
+  uint16_t* pkeys = reinterpret_cast<uint16_t*>(ws + L.pkeys);
 
   int e = launch_normalise(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, rinv, hilo, stream);
   if (e) return hip_status(e);
-  e = launch_partition(retained, rinv, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT, pcol, rcol, pmeta,
-                       status, stream);
+  e = launch_partition(retained, rinv, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT, pcol, rcol, prank,
+                       pmeta, status, stream);
   if (e) return hip_status(e);
 
   SimArgs a;
@@ -166,9 +173,18 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
     a.head_stride = head_stride;
     a.token_stride = token_stride;
   }
+  int max_len = 0;
+  for (int s = 0; s < bt.n_seqs; ++s) max_len = std::max(max_len, (int)(cu[s + 1] - cu[s]));
+  const int dcol = dtype == TWINKV_F32 ? 2 * d : d;
+  e = launch_gather_columns(reinterpret_cast<const uint16_t*>(a.keys), a.head_stride, a.token_stride,
+                            dcol, pcol, pmeta, dtab, bt.n_heads, bt.n_seqs, max_len, bt.PT, pkeys,
+                            stream);
+  if (e) return hip_status(e);
   a.rinv = rinv;
+  a.pkeys = pkeys;
   a.pcol = pcol;
   a.rcol = rcol;
+  a.prank = prank;
   a.pmeta = pmeta;
   a.seqtab = dtab;
   a.n_heads = bt.n_heads;

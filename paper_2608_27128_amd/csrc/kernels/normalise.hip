@@ -97,8 +97,8 @@ constexpr int kPartThreads = 256;
 __global__ __launch_bounds__(kPartThreads) void partition_kernel(
     const uint8_t* __restrict__ retained, const float* __restrict__ rinv,
     const SeqInfo* __restrict__ seqtab, int n_seqs, int64_t T, int64_t PT,
-    int32_t* __restrict__ pcol, float* __restrict__ rcol, ProblemMeta* __restrict__ pmeta,
-    int32_t* __restrict__ status) {
+    int32_t* __restrict__ pcol, float* __restrict__ rcol, int32_t* __restrict__ prank,
+    ProblemMeta* __restrict__ pmeta, int32_t* __restrict__ status) {
   __shared__ int s_red[kPartThreads / 64];
   __shared__ int s_wave[kPartThreads / 64];
   const int q = blockIdx.x;
@@ -110,6 +110,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
   const float* rv = rinv + h * T + si.start;
   int32_t* pc = pcol + h * PT + si.perm_off;
   float* rc = rcol + h * PT + si.perm_off;
+  int32_t* pr = prank + h * PT + si.perm_off;
 
   int cnt = 0, bad = 0;
   for (int t = threadIdx.x; t < len; t += kPartThreads) {
@@ -145,6 +146,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
       const int p = r ? ret_before : ret_pad + (t - ret_before);
       pc[p] = t;
       rc[p] = rv[t];
+      pr[t] = ret_before;
     }
     ret_before_round += tot;
     __syncthreads();
@@ -158,6 +160,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
     rc[k] = 0.0f;
   }
   if (threadIdx.x == 0) {
+    pr[len] = n_ret;
     ProblemMeta m;
     m.n_ret = n_ret;
     m.ret_chunks = ret_pad / kChunk;
@@ -166,6 +169,30 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
     pmeta[q] = m;
     if (status) status[q] = any_bad ? 2 /* TWINKV_PROBLEM_NONFINITE */ : 0;
   }
+}
+
+// K1c: one 16-byte piece per thread; blockIdx.y = problem, blockIdx.x = group of columns.
+constexpr int kGatherThreads = 256;
+
+__global__ __launch_bounds__(kGatherThreads) void gather_columns_kernel(
+    const uint16_t* __restrict__ src, int64_t src_hs, int64_t src_ts, int dcol,
+    const int32_t* __restrict__ pcol, const ProblemMeta* __restrict__ pmeta,
+    const SeqInfo* __restrict__ seqtab, int n_seqs, int64_t PT, uint16_t* __restrict__ pkeys) {
+  const int q = blockIdx.y;
+  const int h = q / n_seqs;
+  const int s = q - h * n_seqs;
+  const SeqInfo si = seqtab[s];
+  const int ncols = pmeta[q].total_chunks * kChunk;
+  const int pieces = dcol / 8;                      // 16-byte pieces per column
+  const int cols_per_block = kGatherThreads / pieces;
+  const int c = blockIdx.x * cols_per_block + threadIdx.x / pieces;
+  const int part = threadIdx.x % pieces;
+  if (c >= ncols) return;
+  const int64_t p = h * PT + si.perm_off + c;
+  const int j = pcol[p];
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (j >= 0) v = *reinterpret_cast<const uint4*>(src + h * src_hs + (int64_t)(si.start + j) * src_ts + part * 8);
+  *reinterpret_cast<uint4*>(pkeys + p * dcol + part * 8) = v;
 }
 
 template <int D, bool F32>
@@ -197,12 +224,27 @@ int launch_normalise(const void* keys, int dtype, int d, int n_heads, int64_t T,
 
 int launch_partition(const uint8_t* retained, const float* rinv, const SeqInfo* seqtab,
                      int n_heads, int n_seqs, int64_t T, int64_t PT, int32_t* pcol, float* rcol,
-                     ProblemMeta* pmeta, int32_t* status, void* stream) {
+                     int32_t* prank, ProblemMeta* pmeta, int32_t* status, void* stream) {
   const int64_t P = (int64_t)n_heads * n_seqs;
   if (P == 0) return hipSuccess;
   hipLaunchKernelGGL(partition_kernel, dim3((unsigned)P), dim3(kPartThreads), 0,
                      (hipStream_t)stream, retained, rinv, seqtab, n_seqs, T, PT, pcol, rcol,
-                     pmeta, status);
+                     prank, pmeta, status);
+  return hipGetLastError();
+}
+
+int launch_gather_columns(const uint16_t* src, int64_t src_head_stride, int64_t src_token_stride,
+                          int dcol, const int32_t* pcol, const ProblemMeta* pmeta,
+                          const SeqInfo* seqtab, int n_heads, int n_seqs, int max_len, int64_t PT,
+                          uint16_t* pkeys, void* stream) {
+  const int64_t P = (int64_t)n_heads * n_seqs;
+  if (P == 0 || max_len == 0) return hipSuccess;
+  const int cols_per_block = kGatherThreads / (dcol / 8);
+  const int max_cols = max_len + kPermPad;
+  const unsigned gx = (unsigned)((max_cols + cols_per_block - 1) / cols_per_block);
+  hipLaunchKernelGGL(gather_columns_kernel, dim3(gx, (unsigned)P), dim3(kGatherThreads), 0,
+                     (hipStream_t)stream, src, src_head_stride, src_token_stride, dcol, pcol, pmeta,
+                     seqtab, n_seqs, PT, pkeys);
   return hipGetLastError();
 }
 

@@ -10,9 +10,9 @@
 //  * One workgroup owns RB = NWAVES * NSUB * 32 consecutive rows of one problem; each wave
 //    holds NSUB 32-row blocks of its row keys as MFMA B operands in registers for the whole
 //    sweep (d <= 128 makes this a short-K contraction).
-//  * Column keys stream through LDS in tiles of TN = 32 * CPT columns, double buffered, in
-//    the partitioned order [S0 | evicted] written by K1b, so every 32-column chunk belongs to
-//    exactly one of the two reductions.
+//  * Column keys stream through LDS in tiles of TN = 32 * CPT columns, double buffered, from
+//    the contiguous copy in partitioned order [S0 | evicted] (K1b, K1c), so every 32-column
+//    chunk belongs to exactly one of the two reductions and tile loads are plain streams.
 //  * v_mfma_f32_32x32x16_bf16 with A = 32 column keys, B = 32 row keys gives each lane one
 //    row i (lane % 32) and 16 columns: register v holds column 8*(v/4) + 4*(lane/32) + v%4.
 //  * Row keys are pre-scaled by an exact power of two g_i so that ||g_i k_i|| is in (0.5, 1];
@@ -23,8 +23,9 @@
 //  * Products of bf16 values are exact in fp32; accumulation is fp32.  fp32 keys use the
 //    split k = hi + lo (bf16 each) and the three products hi.hi + lo.hi + hi.lo, laid out
 //    as a contraction over 3d.
-//  * Pairs inside the window and padding columns only occur in a few chunks per wave; those
-//    take a masked epilogue, all others a 2.6-instruction-per-element epilogue.
+//  * Pairs inside the window and padding columns only occur in a few chunks per wave, found
+//    by scalar range tests; those take a masked epilogue, all others a 2.5-instruction-per-
+//    element epilogue (v_fmaak, v_and_or, half a v_max3).
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"
@@ -142,17 +143,45 @@ __global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
   const int ncols = nchunks * kChunk;
   const int ntiles = (nchunks + CPT - 1) / CPT;
 
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int half = lane >> 5;
   const int l32 = lane & 31;
   const int wrow0 = rb * C::RB + wave * NSUB * 32;
 
+  const int64_t colbase = (int64_t)head * a.PT + si.perm_off;
   const uint16_t* kb = (const uint16_t*)a.keys + (int64_t)head * a.head_stride +
                        (int64_t)si.start * a.token_stride;
-  const int32_t* pc = a.pcol + (int64_t)head * a.PT + si.perm_off;
-  const float* rc = a.rcol + (int64_t)head * a.PT + si.perm_off;
+  const uint16_t* pk = a.pkeys + colbase * C::DCOL;
+  const int32_t* pc = a.pcol + colbase;
+  const float* rc = a.rcol + colbase;
   const float* rinv = a.rinv + (int64_t)head * a.T + si.start;
+
+  // ---- chunks that need the masked epilogue: the window band of this wave's rows and the
+  // padding at the end of each group.  In the [S0 | evicted] order the columns j with
+  // x0 <= j < x1 occupy one contiguous range per group, read off the S0 prefix counts.
+  int cr_lo, cr_hi, ce_lo, ce_hi, pad_r, pad_e;
+  {
+    const int32_t* prk = a.prank + colbase;
+    const int x0 = min(max(wrow0 - a.w, 0), len);
+    const int x1 = min(max(wrow0 + NSUB * 32 + a.w, 0), len);
+    const int r0 = prk[x0], r1 = prk[x1];
+    const int ret_pad = pm.ret_chunks * kChunk;
+    const int e0 = ret_pad + (x0 - r0), e1 = ret_pad + (x1 - r1);
+    cr_lo = r0 < r1 ? r0 / kChunk : 1;
+    cr_hi = r0 < r1 ? (r1 - 1) / kChunk : 0;
+    ce_lo = e0 < e1 ? e0 / kChunk : 1;
+    ce_hi = e0 < e1 ? (e1 - 1) / kChunk : 0;
+    const int n_ev = len - pm.n_ret;
+    pad_r = (pm.n_ret % kChunk) ? pm.n_ret / kChunk : -1;
+    pad_e = (n_ev % kChunk) ? (ret_pad + n_ev) / kChunk : -1;
+    cr_lo = __builtin_amdgcn_readfirstlane(cr_lo);
+    cr_hi = __builtin_amdgcn_readfirstlane(cr_hi);
+    ce_lo = __builtin_amdgcn_readfirstlane(ce_lo);
+    ce_hi = __builtin_amdgcn_readfirstlane(ce_hi);
+    pad_r = __builtin_amdgcn_readfirstlane(pad_r);
+    pad_e = __builtin_amdgcn_readfirstlane(pad_e);
+  }
 
   // ---- row keys: MFMA B operands, resident for the whole sweep ------------------------
   bf16x8 bfrag[NSUB][C::KSTEPS];
@@ -180,37 +209,24 @@ __global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
     cid_e[s] = 0;
   }
 
-  // ---- column tiles: global -> registers -> LDS, double buffered -----------------------
-  // The column index list is read one tile ahead of the key rows it addresses, so the
-  // dependent key loads of tile t+1 never wait on the index loads.
-  int jseg[C::SEGS_PER_THREAD];       // column of each 16-byte piece, next tile to copy
-  int cur_p = -1, nxt_p = -1;         // column index / inverse norm of this thread's column
-  float cur_r = 0.0f, nxt_r = 0.0f;
+  // ---- column tiles: contiguous global rows -> registers -> LDS, double buffered --------
   uint4 pre[C::SEGS_PER_THREAD];
-  auto load_cols = [&](int tile) {
+  int pre_p = -1;
+  float pre_r = 0.0f;
+  auto load_tile = [&](int tile) {
 #pragma unroll
     for (int e = 0; e < C::SEGS_PER_THREAD; ++e) {
       const int seg = threadIdx.x + e * C::NT;
-      const int p = tile * C::TN + seg / C::SEGS_PER_COL;
-      jseg[e] = p < ncols ? pc[p] : -1;
+      const int col = tile * C::TN + seg / C::SEGS_PER_COL;
+      pre[e] = make_uint4(0, 0, 0, 0);
+      if (col < ncols)
+        pre[e] = *reinterpret_cast<const uint4*>(pk + (int64_t)tile * C::TN * C::DCOL + seg * 8);
     }
     if (threadIdx.x < C::TN) {
-      const int p = tile * C::TN + threadIdx.x;
-      nxt_p = p < ncols ? pc[p] : -1;
-      nxt_r = p < ncols ? rc[p] : 0.0f;
+      const int col = tile * C::TN + threadIdx.x;
+      pre_p = col < ncols ? pc[col] : -1;
+      pre_r = col < ncols ? rc[col] : 0.0f;
     }
-  };
-  auto load_keys = [&]() {
-#pragma unroll
-    for (int e = 0; e < C::SEGS_PER_THREAD; ++e) {
-      const int seg = threadIdx.x + e * C::NT;
-      const int part = seg - (seg / C::SEGS_PER_COL) * C::SEGS_PER_COL;
-      pre[e] = make_uint4(0, 0, 0, 0);
-      if (jseg[e] >= 0)
-        pre[e] = *reinterpret_cast<const uint4*>(kb + (int64_t)jseg[e] * a.token_stride + part * 8);
-    }
-    cur_p = nxt_p;
-    cur_r = nxt_r;
   };
   auto store_tile = [&](int buf) {
     char* st = smem + buf * C::STAGE;
@@ -225,55 +241,74 @@ __global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
       *reinterpret_cast<uint4*>(lk + lc * C::STRIDE + part * 8) = pre[e];
     }
     if (threadIdx.x < C::TN) {
-      lr[threadIdx.x] = cur_r;
-      lp[threadIdx.x] = cur_p;
+      lr[threadIdx.x] = pre_r;
+      lp[threadIdx.x] = pre_p;
     }
   };
 
   if (ntiles > 0) {
-    load_cols(0);
-    load_keys();
+    load_tile(0);
     store_tile(0);
-    if (ntiles > 1) load_cols(1);
   }
   __syncthreads();
 
-  const int band_lo = wrow0 - a.w;                 // columns with j >= band_lo and
-  const int band_hi = wrow0 + NSUB * 32 - 1 + a.w; // j <= band_hi may fall inside a window
-
   for (int tile = 0; tile < ntiles; ++tile) {
-    if (tile + 1 < ntiles) {
-      load_keys();
-      if (tile + 2 < ntiles) load_cols(tile + 2);
-    }
+    if (tile + 1 < ntiles) load_tile(tile + 1);
     const char* st = smem + (tile & 1) * C::STAGE;
     const uint16_t* lk = reinterpret_cast<const uint16_t*>(st);
     const float* lr = reinterpret_cast<const float*>(st + C::KEY_BYTES);
     const int* lp = reinterpret_cast<const int*>(st + C::KEY_BYTES + C::TN * 4);
+
+    // A operands and column inverse norms of chunk c, read from LDS one chunk ahead
+    bf16x8 af[C::KSTEPS];
+    float rv[16];
+    auto read_chunk = [&](int c, bf16x8 (&dst)[C::KSTEPS], float (&rdst)[16]) {
+      const int col = c * kChunk + l32;
+#pragma unroll
+      for (int t = 0; t < C::KSTEPS; ++t)
+        dst[t] = *reinterpret_cast<const bf16x8*>(lk + col * C::STRIDE + col_off<D, SPLIT>(t) + half * 8);
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 x = *reinterpret_cast<const float4*>(lr + c * kChunk + 8 * g4 + 4 * half);
+        rdst[4 * g4 + 0] = x.x;
+        rdst[4 * g4 + 1] = x.y;
+        rdst[4 * g4 + 2] = x.z;
+        rdst[4 * g4 + 3] = x.w;
+      }
+    };
+    read_chunk(0, af, rv);
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       const int gc = tile * CPT + c;
       if (gc >= nchunks) break;
-      bf16x8 af[C::KSTEPS];
-      const int col = c * kChunk + l32;
-#pragma unroll
-      for (int t = 0; t < C::KSTEPS; ++t)
-        af[t] = *reinterpret_cast<const bf16x8*>(lk + col * C::STRIDE + col_off<D, SPLIT>(t) + half * 8);
-      float rv[16];
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const float4 x = *reinterpret_cast<const float4*>(lr + c * kChunk + 8 * g4 + 4 * half);
-        rv[4 * g4 + 0] = x.x;
-        rv[4 * g4 + 1] = x.y;
-        rv[4 * g4 + 2] = x.z;
-        rv[4 * g4 + 3] = x.w;
-      }
-      const int first = lp[c * kChunk];
-      const int last = lp[c * kChunk + kChunk - 1];
-      const bool slow = (last < 0) || (first <= band_hi && last >= band_lo);
+      bf16x8 afn[C::KSTEPS];
+      float rvn[16];
+      if (c + 1 < CPT) read_chunk(c + 1, afn, rvn);
+      const bool slow = (gc >= cr_lo && gc <= cr_hi) || (gc >= ce_lo && gc <= ce_hi) ||
+                        gc == pad_r || gc == pad_e;
       const bool in_ret = gc < pm.ret_chunks;
-      int jv[16];
-      if (slow) {
+      f32x16 acc[NSUB];
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        acc[s] = f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < C::KSTEPS; ++t)
+          acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], acc[s], 0, 0, 0);
+      }
+      uint32_t best[NSUB];
+      if (!slow) {
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+          uint32_t b = 0u;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float x = fmaf(acc[s][v], rv[v], 3.0f);
+            b = max(b, (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v));
+          }
+          best[s] = b;
+        }
+      } else {
+        int jv[16];
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
           const int4 x = *reinterpret_cast<const int4*>(lp + c * kChunk + 8 * g4 + 4 * half);
@@ -282,38 +317,34 @@ __global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
           jv[4 * g4 + 2] = x.z;
           jv[4 * g4 + 3] = x.w;
         }
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+          const int i = wrow0 + s * 32 + l32;
+          uint32_t b = 0u;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float x = fmaf(acc[s][v], rv[v], 3.0f);
+            const uint32_t u = (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
+            const bool ok = (jv[v] >= 0) && (abs(i - jv[v]) > a.w);
+            b = max(b, ok ? u : 0u);
+          }
+          best[s] = b;
+        }
       }
+      // strictly larger value (slot bits ignored): an earlier chunk keeps exact ties
 #pragma unroll
       for (int s = 0; s < NSUB; ++s) {
-        f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int t = 0; t < C::KSTEPS; ++t)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], acc, 0, 0, 0);
-        uint32_t best = 0u;
-        if (!slow) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float x = fmaf(acc[v], rv[v], 3.0f);
-            const uint32_t u = (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
-            best = max(best, u);
-          }
-        } else {
-          const int i = wrow0 + s * 32 + l32;
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float x = fmaf(acc[v], rv[v], 3.0f);
-            const uint32_t u = (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
-            const int j = jv[v];
-            const bool ok = (j >= 0) && (abs(i - j) > a.w);
-            best = max(best, ok ? u : 0u);
-          }
-        }
-        // strictly larger value (slot bits ignored): an earlier chunk keeps exact ties
         if (in_ret) {
-          if ((best >> 4) > (run_r[s] >> 4)) { run_r[s] = best; cid_r[s] = gc; }
+          if ((best[s] >> 4) > (run_r[s] >> 4)) { run_r[s] = best[s]; cid_r[s] = gc; }
         } else {
-          if ((best >> 4) > (run_e[s] >> 4)) { run_e[s] = best; cid_e[s] = gc; }
+          if ((best[s] >> 4) > (run_e[s] >> 4)) { run_e[s] = best[s]; cid_e[s] = gc; }
         }
+      }
+      if (c + 1 < CPT) {
+#pragma unroll
+        for (int t = 0; t < C::KSTEPS; ++t) af[t] = afn[t];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) rv[v] = rvn[v];
       }
     }
     if (tile + 1 < ntiles) store_tile((tile + 1) & 1);
@@ -377,8 +408,8 @@ hipError_t run(const SimArgs& a, hipStream_t st) {
 }  // namespace
 
 // Tile shapes: (NSUB 32-row blocks per wave, waves per workgroup, 32-column chunks per tile).
-#define TWINKV_CFG_BF16_128 128, false, 2, 8, 2
-#define TWINKV_CFG_BF16_64 64, false, 4, 8, 2
+#define TWINKV_CFG_BF16_128 128, false, 2, 8, 4
+#define TWINKV_CFG_BF16_64 64, false, 4, 8, 4
 #define TWINKV_CFG_F32_64 64, true, 2, 4, 2
 #define TWINKV_CFG_F32_128 128, true, 1, 4, 1
 

@@ -35,7 +35,8 @@ constexpr int kFlagNonfinite = 1;
 
 // Workspace layout shared by the size query and the launchers.
 struct Layout {
-  size_t seqtab = 0, rinv = 0, pcol = 0, rcol = 0, pmeta = 0, hilo = 0, bbuf = 0;
+  size_t seqtab = 0, rinv = 0, pcol = 0, rcol = 0, prank = 0, pmeta = 0, hilo = 0, pkeys = 0,
+         bbuf = 0;
   size_t total = 0;
 };
 
@@ -49,18 +50,28 @@ int launch_normalise(const void* keys, int dtype, int d, int n_heads, int64_t T,
                      void* stream);
 
 // K1b: stable partition of each problem's positions into [S0 | evicted] column lists,
-// padded to whole chunks, with the inverse norm of every listed column.
+// padded to whole chunks, with the inverse norm of every listed column, and
+// prank[t] = number of S0 positions before t (t = 0..len) per problem.
 int launch_partition(const uint8_t* retained, const float* rinv, const SeqInfo* seqtab,
                      int n_heads, int n_seqs, int64_t T, int64_t PT, int32_t* pcol, float* rcol,
-                     ProblemMeta* pmeta, int32_t* status, void* stream);
+                     int32_t* prank, ProblemMeta* pmeta, int32_t* status, void* stream);
+
+// K1c: copy of the column keys in partitioned order, pkeys[h][PT][dcol] (bf16; padding zero).
+// src/src_head_stride/src_token_stride in uint16 elements; dcol = d (bf16) or 2d (hi/lo).
+int launch_gather_columns(const uint16_t* src, int64_t src_head_stride, int64_t src_token_stride,
+                          int dcol, const int32_t* pcol, const ProblemMeta* pmeta,
+                          const SeqInfo* seqtab, int n_heads, int n_seqs, int max_len, int64_t PT,
+                          uint16_t* pkeys, void* stream);
 
 struct SimArgs {
   const void* keys;          // bf16 keys, or the hi/lo planes for fp32 keys
   int64_t head_stride;       // elements (of uint16) between heads of `keys`
   int64_t token_stride;      // elements between tokens of `keys`
   const float* rinv;         // [n_heads][T]
+  const uint16_t* pkeys;     // [n_heads][PT][dcol] column keys in partitioned order
   const int32_t* pcol;       // [n_heads][PT]
   const float* rcol;         // [n_heads][PT]
+  const int32_t* prank;      // [n_heads][PT]: S0 positions before t
   const ProblemMeta* pmeta;  // [n_heads * n_seqs]
   const SeqInfo* seqtab;     // [n_seqs]
   int n_heads, n_seqs;
