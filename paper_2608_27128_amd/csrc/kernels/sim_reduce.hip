@@ -28,6 +28,8 @@
 //    element epilogue (v_fmaak, v_and_or, half a v_max3).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "../twinkv_internal.h"
 
 namespace twinkv {
@@ -40,16 +42,17 @@ template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
 struct Cfg {
   static constexpr int KSTEPS = SPLIT ? 3 * D / 16 : D / 16;
   static constexpr int DCOL = SPLIT ? 2 * D : D;      // bf16 elements per column in LDS
-  static constexpr int STRIDE = DCOL + 8;             // +16 bytes against bank conflicts
-  static constexpr int TN = CPT * kChunk;
-  static constexpr int SEGS_PER_COL = DCOL / 8;       // 16-byte pieces per column
+  static constexpr int PPC = DCOL / 8;                // 16-byte pieces per column
+  static constexpr int SWZ = (PPC < 16 ? PPC : 16) - 1;  // piece-index XOR swizzle mask
+  static constexpr int TN = CPT * kChunk;             // columns per LDS tile
   static constexpr int NT = NWAVES * 64;
-  static constexpr int SEGS = TN * SEGS_PER_COL;
-  static constexpr int SEGS_PER_THREAD = SEGS / NT;
-  static constexpr int RB = NWAVES * NSUB * 32;
-  static constexpr int KEY_BYTES = TN * STRIDE * 2;
-  static constexpr int STAGE = KEY_BYTES + TN * 4 + TN * 4;
-  static_assert(SEGS % NT == 0, "tile copy must divide evenly");
+  static constexpr int RB = NWAVES * NSUB * 32;       // rows per workgroup
+  static constexpr int KEY_BYTES = TN * DCOL * 2;
+  static constexpr int STAGE = KEY_BYTES + TN * 8;    // keys + inverse norms + positions
+  static constexpr int RETIRED = NWAVES * NSUB * 64 * 8;  // S0 results parked in LDS
+  static constexpr int LOADS_PER_WAVE = TN * PPC / (NWAVES * 64);  // 1-KB direct loads
+  static constexpr int VALU_PER_MFMA = (52 + KSTEPS - 1) / KSTEPS;
+  static_assert((TN * PPC) % (NWAVES * 64) == 0, "tile copy must divide evenly");
   static_assert(TN <= NT, "one thread per tile column for the column tables");
 };
 
@@ -102,10 +105,34 @@ __device__ inline int slot_col(int v, int half) { return 8 * (v >> 2) + 4 * half
 
 constexpr uint32_t kValidMin = 0x3F800000u;  // packed values >= 1.0f are real candidates
 
+// Scheduling-group masks for __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedValu = 0x002;
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
+
+// Value + slot of the best column of one lane's 16 accumulators (unmasked chunk).
+__device__ inline uint32_t chunk_best(const f32x16& acc, const float (&rv)[16]) {
+  uint32_t b = 0u;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const float x = fmaf(acc[v], rv[v], 3.0f);
+    b = max(b, (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v));
+  }
+  return b;
+}
+
+// Branch-free running update: a strictly larger value (slot bits ignored) replaces the
+// running best, so an earlier chunk keeps exact ties.
+__device__ inline void run_update(uint32_t best, int gc, uint32_t& run, int& cid) {
+  const bool upd = (best >> 4) > (run >> 4);
+  run = upd ? best : run;
+  cid = upd ? gc : cid;
+}
+
 template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
-__global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
+__global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
   using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT>;
-  __shared__ __attribute__((aligned(16))) char smem[2 * C::STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE + C::RETIRED];
 
   // ---- which (head, sequence, row block) this workgroup owns --------------------------
   // With >= 8 heads, heads h = x (mod 8) go to the XCD x the hardware dispatches block
@@ -144,6 +171,7 @@ __global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
   const int ntiles = (nchunks + CPT - 1) / CPT;
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint2* retired = reinterpret_cast<uint2*>(smem + 2 * C::STAGE) + wave * NSUB * 64;
   const int lane = threadIdx.x & 63;
   const int half = lane >> 5;
   const int l32 = lane & 31;
@@ -196,160 +224,160 @@ __global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
       if (ok) raw = *reinterpret_cast<const uint4*>(kb + (int64_t)i * a.token_stride +
                                                      row_off<D, SPLIT>(t) + half * 8);
       bfrag[s][t] = scale8(raw, g);
+      // Row keys are only ever MFMA operands: keep them in accumulation registers so the
+      // architectural VGPRs stay free for the epilogue (MFMA reads srcB from AGPRs).
+      asm volatile("" : "+a"(bfrag[s][t]));
     }
   }
 
-  uint32_t run_r[NSUB], run_e[NSUB];
-  int cid_r[NSUB], cid_e[NSUB];
+  // One running maximum per row block: S0 columns are swept first, and their results are
+  // parked in LDS (``retire``) when the sweep reaches the evicted columns.
+  uint32_t run[NSUB];
+  int cid[NSUB];
 #pragma unroll
   for (int s = 0; s < NSUB; ++s) {
-    run_r[s] = 0u;
-    run_e[s] = 0u;
-    cid_r[s] = 0;
-    cid_e[s] = 0;
+    run[s] = 0u;
+    cid[s] = 0;
   }
-
-  // ---- column tiles: contiguous global rows -> registers -> LDS, double buffered --------
-  uint4 pre[C::SEGS_PER_THREAD];
-  int pre_p = -1;
-  float pre_r = 0.0f;
-  auto load_tile = [&](int tile) {
+  bool retired_done = false;
+  auto retire = [&]() {
 #pragma unroll
-    for (int e = 0; e < C::SEGS_PER_THREAD; ++e) {
-      const int seg = threadIdx.x + e * C::NT;
-      const int col = tile * C::TN + seg / C::SEGS_PER_COL;
-      pre[e] = make_uint4(0, 0, 0, 0);
-      if (col < ncols)
-        pre[e] = *reinterpret_cast<const uint4*>(pk + (int64_t)tile * C::TN * C::DCOL + seg * 8);
+    for (int s = 0; s < NSUB; ++s) {
+      retired[s * 64 + lane] = make_uint2(run[s], (uint32_t)cid[s]);
+      run[s] = 0u;
+      cid[s] = 0;
+    }
+    retired_done = true;
+  };
+
+  // ---- column tiles: global -> LDS by direct (asynchronous) loads, double buffered ------
+  // Each wave moves LOADS_PER_WAVE blocks of 1 KB; lane l of a block lands at byte 16*l.
+  // A column's 16-byte piece p is stored in slot p ^ (column & SWZ) of its row, so the
+  // 32 lanes that read one piece of 32 consecutive columns hit distinct banks.
+  int nxt_p = -1;
+  float nxt_r = 0.0f;
+  auto issue_tile = [&](int tile, int buf) {
+    char* st = smem + buf * C::STAGE;
+#pragma unroll
+    for (int kk = 0; kk < C::LOADS_PER_WAVE; ++kk) {
+      const int blk = wave * C::LOADS_PER_WAVE + kk;
+      const int e = blk * 64 + lane;
+      const int col = e / C::PPC;
+      const int slot = e - col * C::PPC;
+      const int part = slot ^ (col & C::SWZ);
+      int gcol = tile * C::TN + col;
+      gcol = gcol < ncols ? gcol : 0;            // beyond the last chunk: any valid column
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(pk + (int64_t)gcol * C::DCOL + part * 8),
+          (void __attribute__((address_space(3)))*)(st + blk * 1024), 16, 0, 0);
     }
     if (threadIdx.x < C::TN) {
       const int col = tile * C::TN + threadIdx.x;
-      pre_p = col < ncols ? pc[col] : -1;
-      pre_r = col < ncols ? rc[col] : 0.0f;
+      nxt_p = col < ncols ? pc[col] : -1;
+      nxt_r = col < ncols ? rc[col] : 0.0f;
     }
   };
-  auto store_tile = [&](int buf) {
+  auto finish_tile = [&](int buf) {  // column tables of the issued tile, then wait for all
     char* st = smem + buf * C::STAGE;
-    uint16_t* lk = reinterpret_cast<uint16_t*>(st);
-    float* lr = reinterpret_cast<float*>(st + C::KEY_BYTES);
-    int* lp = reinterpret_cast<int*>(st + C::KEY_BYTES + C::TN * 4);
-#pragma unroll
-    for (int e = 0; e < C::SEGS_PER_THREAD; ++e) {
-      const int seg = threadIdx.x + e * C::NT;
-      const int lc = seg / C::SEGS_PER_COL;
-      const int part = seg - lc * C::SEGS_PER_COL;
-      *reinterpret_cast<uint4*>(lk + lc * C::STRIDE + part * 8) = pre[e];
-    }
     if (threadIdx.x < C::TN) {
-      lr[threadIdx.x] = pre_r;
-      lp[threadIdx.x] = pre_p;
+      reinterpret_cast<float*>(st + C::KEY_BYTES)[threadIdx.x] = nxt_r;
+      reinterpret_cast<int*>(st + C::KEY_BYTES + C::TN * 4)[threadIdx.x] = nxt_p;
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
 
   if (ntiles > 0) {
-    load_tile(0);
-    store_tile(0);
+    issue_tile(0, 0);
+    finish_tile(0);
   }
   __syncthreads();
 
   for (int tile = 0; tile < ntiles; ++tile) {
-    if (tile + 1 < ntiles) load_tile(tile + 1);
+    if (tile + 1 < ntiles) issue_tile(tile + 1, (tile + 1) & 1);
     const char* st = smem + (tile & 1) * C::STAGE;
     const uint16_t* lk = reinterpret_cast<const uint16_t*>(st);
     const float* lr = reinterpret_cast<const float*>(st + C::KEY_BYTES);
     const int* lp = reinterpret_cast<const int*>(st + C::KEY_BYTES + C::TN * 4);
 
-    // A operands and column inverse norms of chunk c, read from LDS one chunk ahead
-    bf16x8 af[C::KSTEPS];
-    float rv[16];
-    auto read_chunk = [&](int c, bf16x8 (&dst)[C::KSTEPS], float (&rdst)[16]) {
+    // One 32-column chunk: the MFMA chain of 32-row block s runs while the VALU reduces
+    // block s - 1.  RET picks the running maximum, MASKED applies the window / padding test.
+    auto chunk = [&](int c, int gc, auto mask_tag) {
+      constexpr bool MASKED = decltype(mask_tag)::value;
       const int col = c * kChunk + l32;
+      bf16x8 af[C::KSTEPS];
 #pragma unroll
-      for (int t = 0; t < C::KSTEPS; ++t)
-        dst[t] = *reinterpret_cast<const bf16x8*>(lk + col * C::STRIDE + col_off<D, SPLIT>(t) + half * 8);
+      for (int t = 0; t < C::KSTEPS; ++t) {
+        const int part = (col_off<D, SPLIT>(t) >> 3) + half;
+        af[t] = *reinterpret_cast<const bf16x8*>(lk + col * C::DCOL + ((part ^ (col & C::SWZ)) << 3));
+      }
+      float rv[16];
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const float4 x = *reinterpret_cast<const float4*>(lr + c * kChunk + 8 * g4 + 4 * half);
-        rdst[4 * g4 + 0] = x.x;
-        rdst[4 * g4 + 1] = x.y;
-        rdst[4 * g4 + 2] = x.z;
-        rdst[4 * g4 + 3] = x.w;
+        rv[4 * g4 + 0] = x.x;
+        rv[4 * g4 + 1] = x.y;
+        rv[4 * g4 + 2] = x.z;
+        rv[4 * g4 + 3] = x.w;
       }
-    };
-    read_chunk(0, af, rv);
+      auto reduce = [&](const f32x16& acc, int s) {
+        uint32_t best;
+        if constexpr (MASKED) {
+          // column positions read here (rare path) so they are not live across the chunk
+          const int i = wrow0 + s * 32 + l32;
+          best = 0u;
 #pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int4 jq = *reinterpret_cast<const int4*>(lp + c * kChunk + 8 * g4 + 4 * half);
+            const int jv[4] = {jq.x, jq.y, jq.z, jq.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int v = 4 * g4 + q;
+              const float y = fmaf(acc[v], rv[v], 3.0f);
+              const uint32_t u = (__float_as_uint(y) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
+              const bool ok = (jv[q] >= 0) && (abs(i - jv[q]) > a.w);
+              best = max(best, ok ? u : 0u);
+            }
+          }
+        } else {
+          best = chunk_best(acc, rv);
+        }
+        run_update(best, gc, run[s], cid[s]);
+      };
+      f32x16 prev;
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        f32x16 x = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < C::KSTEPS; ++t)
+          x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], x, 0, 0, 0);
+        if (s > 0) reduce(prev, s - 1);
+        prev = x;
+        if (s > 0) {
+#pragma unroll
+          for (int i = 0; i < C::KSTEPS; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedValu, C::VALU_PER_MFMA, 0);
+          }
+        }
+      }
+      reduce(prev, NSUB - 1);
+    };
+
+#pragma unroll 1
     for (int c = 0; c < CPT; ++c) {
       const int gc = tile * CPT + c;
       if (gc >= nchunks) break;
-      bf16x8 afn[C::KSTEPS];
-      float rvn[16];
-      if (c + 1 < CPT) read_chunk(c + 1, afn, rvn);
-      const bool slow = (gc >= cr_lo && gc <= cr_hi) || (gc >= ce_lo && gc <= ce_hi) ||
-                        gc == pad_r || gc == pad_e;
-      const bool in_ret = gc < pm.ret_chunks;
-      f32x16 acc[NSUB];
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s) {
-        acc[s] = f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int t = 0; t < C::KSTEPS; ++t)
-          acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], acc[s], 0, 0, 0);
-      }
-      uint32_t best[NSUB];
-      if (!slow) {
-#pragma unroll
-        for (int s = 0; s < NSUB; ++s) {
-          uint32_t b = 0u;
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float x = fmaf(acc[s][v], rv[v], 3.0f);
-            b = max(b, (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v));
-          }
-          best[s] = b;
-        }
-      } else {
-        int jv[16];
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const int4 x = *reinterpret_cast<const int4*>(lp + c * kChunk + 8 * g4 + 4 * half);
-          jv[4 * g4 + 0] = x.x;
-          jv[4 * g4 + 1] = x.y;
-          jv[4 * g4 + 2] = x.z;
-          jv[4 * g4 + 3] = x.w;
-        }
-#pragma unroll
-        for (int s = 0; s < NSUB; ++s) {
-          const int i = wrow0 + s * 32 + l32;
-          uint32_t b = 0u;
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float x = fmaf(acc[s][v], rv[v], 3.0f);
-            const uint32_t u = (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
-            const bool ok = (jv[v] >= 0) && (abs(i - jv[v]) > a.w);
-            b = max(b, ok ? u : 0u);
-          }
-          best[s] = b;
-        }
-      }
-      // strictly larger value (slot bits ignored): an earlier chunk keeps exact ties
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s) {
-        if (in_ret) {
-          if ((best[s] >> 4) > (run_r[s] >> 4)) { run_r[s] = best[s]; cid_r[s] = gc; }
-        } else {
-          if ((best[s] >> 4) > (run_e[s] >> 4)) { run_e[s] = best[s]; cid_e[s] = gc; }
-        }
-      }
-      if (c + 1 < CPT) {
-#pragma unroll
-        for (int t = 0; t < C::KSTEPS; ++t) af[t] = afn[t];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) rv[v] = rvn[v];
-      }
+      if (gc == pm.ret_chunks) retire();
+      const bool masked = (gc >= cr_lo && gc <= cr_hi) || (gc >= ce_lo && gc <= ce_hi) ||
+                          gc == pad_r || gc == pad_e;
+      if (!masked) chunk(c, gc, std::false_type{});
+      else chunk(c, gc, std::true_type{});
     }
-    if (tile + 1 < ntiles) store_tile((tile + 1) & 1);
+    if (tile + 1 < ntiles) finish_tile((tile + 1) & 1);
     __syncthreads();
   }
+
+  if (!retired_done) retire();          // no evicted columns were swept
 
   // ---- resolve: lanes l and l+32 hold the same row over disjoint column halves ----------
 #pragma unroll
@@ -359,8 +387,9 @@ __global__ __launch_bounds__(NWAVES * 64) void sim_reduce_kernel(SimArgs a) {
     const float g = row_scale(ri);
     uint32_t val[2];
     int pos[2];
-    const uint32_t runs[2] = {run_r[s], run_e[s]};
-    const int cids[2] = {cid_r[s], cid_e[s]};
+    const uint2 rr = retired[s * 64 + lane];
+    const uint32_t runs[2] = {rr.x, run[s]};
+    const int cids[2] = {(int)rr.y, cid[s]};
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
       uint32_t v = runs[grp] & 0xFFFFFFF0u;
@@ -408,10 +437,10 @@ hipError_t run(const SimArgs& a, hipStream_t st) {
 }  // namespace
 
 // Tile shapes: (NSUB 32-row blocks per wave, waves per workgroup, 32-column chunks per tile).
-#define TWINKV_CFG_BF16_128 128, false, 2, 8, 4
-#define TWINKV_CFG_BF16_64 64, false, 4, 8, 4
-#define TWINKV_CFG_F32_64 64, true, 2, 4, 2
-#define TWINKV_CFG_F32_128 128, true, 1, 4, 1
+#define TWINKV_CFG_BF16_128 128, false, 3, 4, 4
+#define TWINKV_CFG_BF16_64 64, false, 4, 4, 4
+#define TWINKV_CFG_F32_64 64, true, 2, 4, 4
+#define TWINKV_CFG_F32_128 128, true, 1, 4, 2
 
 int sim_rows_per_block(int dtype, int d) {
   if (dtype == 0 && d == 128) return Cfg<TWINKV_CFG_BF16_128>::RB;
