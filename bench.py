@@ -87,7 +87,9 @@ def profiled_traffic(workload: str):
 
 
 def cpu_baseline(batch, target_s: float = 15.0) -> dict:
-    """The fp64 oracle on a bounded row sample of problem (head 0, sequence 0)."""
+    """The fp64 oracle on a bounded sample of the same workload: whole problems (all rows,
+    both reductions) in (head, sequence) order, then a row prefix of the next one, until
+    about target_s seconds of CPU work have been done."""
     import numpy as np
     import oracle
     try:
@@ -95,26 +97,32 @@ def cpu_baseline(batch, target_s: float = 15.0) -> dict:
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover - threadpoolctl missing
         cores = os.cpu_count() or 1
-    a, e = int(batch.cu_seqlens[0]), int(batch.cu_seqlens[1])
-    keys, ret = batch.keys[0, a:e], batch.retained[0, a:e]
-    n = e - a
     w = batch.spec.w
-    probe = min(n, 64)
-    while True:                      # grow the probe until it takes a measurable while
+    H, S = batch.n_heads, batch.n_seqs
+    pairs, done, spent = 0.0, [], 0.0
+    rate = None
+    for q in range(H * S):
+        h, s = divmod(q, S)
+        a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
+        n = e - a
+        if n == 0:
+            continue
+        keys, ret = batch.keys[h, a:e], batch.retained[h, a:e]
+        left = target_s - spent
+        rows = n if rate is None else int(min(n, max(1, left * rate / n)))
         t = time.perf_counter()
-        oracle.nn_scores(keys, batch.dtype, ret, w, rows=np.arange(probe))
-        tp = time.perf_counter() - t
-        if tp >= 0.1 * target_s or probe >= n:
+        oracle.nn_scores(keys, batch.dtype, ret, w, rows=np.arange(rows))
+        dt = time.perf_counter() - t
+        spent += dt
+        pairs += rows * n
+        rate = pairs / spent
+        done.append(f"(h{h},s{s}) rows 0..{rows - 1} of {n}")
+        if spent >= 0.9 * target_s:
             break
-        probe = min(n, probe * 4)
-    rows = int(min(n, max(probe, probe * target_s / max(tp, 1e-3))))
-    t = time.perf_counter()
-    oracle.nn_scores(keys, batch.dtype, ret, w, rows=np.arange(rows))
-    dt = time.perf_counter() - t
-    return {"value": rows * n / dt, "unit": "pairs/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"oracle.nn_scores (both reductions, fp64) on rows 0..{rows - 1} of "
-                      f"problem (head 0, seq 0), N={n}, d={batch.d}: {rows * n:.3e} ordered pairs "
-                      f"in {dt:.1f} s"}
+    return {"value": pairs / spent, "unit": "pairs/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"oracle.nn_scores (both reductions, fp64), d={batch.d}: "
+                      f"{'; '.join(done[:3])}{' ...' if len(done) > 3 else ''} "
+                      f"({len(done)} problems), {pairs:.3e} ordered pairs in {spent:.1f} s"}
 
 
 def main() -> int:

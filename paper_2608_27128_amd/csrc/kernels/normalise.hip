@@ -1,7 +1,8 @@
 // K1a: per-key inverse l2 norm (Sec. 3.2: k_hat = k / ||k||_2) and, for fp32 keys, the bf16
 //      hi/lo split the similarity kernel multiplies on bf16 MFMA.
-// K1b: per-problem stable partition of the positions into [S0 | evicted] column lists, each
-//      list padded to whole 32-column chunks, carrying the inverse norm of every column.
+// K1b: per-problem stable partition of the positions into [S0 | evicted] column lists (the
+//      S0 list padded to a multiple of kGroupAlign columns, the evicted list to whole
+//      32-column chunks), carrying the inverse norm of every column.
 //
 // Both kernels are HBM-bound streams: K1a reads d*esize bytes and writes 4 bytes per key
 // (+ 4d bytes of planes for fp32 keys); K1b reads 1 + 4 bytes and writes 8 bytes per key.
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
   }
   const int n_ret = block_sum<kPartThreads>(cnt, s_red);
   const int any_bad = block_sum<kPartThreads>(bad, s_red);
-  const int ret_pad = (n_ret + kChunk - 1) / kChunk * kChunk;
+  const int ret_pad = (n_ret + kGroupAlign - 1) / kGroupAlign * kGroupAlign;
   const int n_ev = len - n_ret;
   const int ev_pad = (n_ev + kChunk - 1) / kChunk * kChunk;
 

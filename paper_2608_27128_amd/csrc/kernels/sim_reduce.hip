@@ -47,11 +47,12 @@ struct Cfg {
   static constexpr int TN = CPT * kChunk;             // columns per LDS tile
   static constexpr int NT = NWAVES * 64;
   static constexpr int RB = NWAVES * NSUB * 32;       // rows per workgroup
+  static constexpr int CHUNK_BYTES = kChunk * DCOL * 2;  // keys of one 32-column chunk
   static constexpr int KEY_BYTES = TN * DCOL * 2;
   static constexpr int STAGE = KEY_BYTES + TN * 8;    // keys + inverse norms + positions
   static constexpr int RETIRED = NWAVES * NSUB * 64 * 8;  // S0 results parked in LDS
   static constexpr int LOADS_PER_WAVE = TN * PPC / (NWAVES * 64);  // 1-KB direct loads
-  static constexpr int VALU_PER_MFMA = (52 + KSTEPS - 1) / KSTEPS;
+  static constexpr int VALU_PER_MFMA = (48 + KSTEPS - 1) / KSTEPS;
   static_assert((TN * PPC) % (NWAVES * 64) == 0, "tile copy must divide evenly");
   static_assert(TN <= NT, "one thread per tile column for the column tables");
 };
@@ -105,6 +106,18 @@ __device__ inline int slot_col(int v, int half) { return 8 * (v >> 2) + 4 * half
 
 constexpr uint32_t kValidMin = 0x3F800000u;  // packed values >= 1.0f are real candidates
 
+// Fourth dword of a raw buffer resource on gfx9-family parts (32-bit data format).
+constexpr int kBufferFlags = 0x00020000;
+
+// 16 bytes per lane from base + voff straight into LDS at lds + 16 * lane, through a raw
+// buffer resource of nbytes: lanes whose offset is past the end read nothing (zeros).
+__device__ inline void load_block_lds(const void* base, int nbytes, int voff, char* lds) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes, kBufferFlags);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void __attribute__((address_space(3)))*)lds, 16,
+                                           voff, 0, 0, 0);
+}
+
 // Scheduling-group masks for __builtin_amdgcn_sched_group_barrier.
 constexpr int kSchedValu = 0x002;
 constexpr int kSchedMfma = 0x008;
@@ -132,6 +145,7 @@ __device__ inline void run_update(uint32_t best, int gc, uint32_t& run, int& cid
 template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
 __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
   using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT>;
+  static_assert(kGroupAlign % C::TN == 0, "the evicted group must start on a tile boundary");
   __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE + C::RETIRED];
 
   // ---- which (head, sequence, row block) this workgroup owns --------------------------
@@ -167,6 +181,8 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
   const ProblemMeta pm = a.pmeta[q];
   const int len = si.len;
   const int nchunks = a.want_all ? pm.total_chunks : pm.ret_chunks;
+  const int ret_chunks = pm.ret_chunks;                      // a multiple of CPT
+  const int ret_real = (pm.n_ret + kChunk - 1) / kChunk;     // S0 chunks with a real column
   const int ncols = nchunks * kChunk;
   const int ntiles = (nchunks + CPT - 1) / CPT;
 
@@ -186,7 +202,7 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
   const float* rinv = a.rinv + (int64_t)head * a.T + si.start;
 
   // ---- chunks that need the masked epilogue: the window band of this wave's rows and the
-  // padding at the end of each group.  In the [S0 | evicted] order the columns j with
+  // partly padded last chunk of each group.  In the [S0 | evicted] order the columns j with
   // x0 <= j < x1 occupy one contiguous range per group, read off the S0 prefix counts.
   int cr_lo, cr_hi, ce_lo, ce_hi, pad_r, pad_e;
   {
@@ -194,7 +210,7 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
     const int x0 = min(max(wrow0 - a.w, 0), len);
     const int x1 = min(max(wrow0 + NSUB * 32 + a.w, 0), len);
     const int r0 = prk[x0], r1 = prk[x1];
-    const int ret_pad = pm.ret_chunks * kChunk;
+    const int ret_pad = ret_chunks * kChunk;
     const int e0 = ret_pad + (x0 - r0), e1 = ret_pad + (x1 - r1);
     cr_lo = r0 < r1 ? r0 / kChunk : 1;
     cr_hi = r0 < r1 ? (r1 - 1) / kChunk : 0;
@@ -210,6 +226,23 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
     pad_r = __builtin_amdgcn_readfirstlane(pad_r);
     pad_e = __builtin_amdgcn_readfirstlane(pad_e);
   }
+  // Result bits of the CPT chunks of a tile in the main sweep (bit k: keep chunk c0 + k).
+  // Dropped: chunks the masked pass redoes, the padding-only chunks that align the S0 group,
+  // and chunks past the last one.  Branch-free scalar arithmetic, so the tile body stays
+  // one straight-line block.
+  auto keep_bits = [&](int c0) -> uint32_t {
+    uint32_t bits = 0u;
+#pragma unroll
+    for (int kc = 0; kc < CPT; ++kc) {
+      const int gc = c0 + kc;
+      const int drop = (int)(gc >= nchunks) | ((int)(gc >= ret_real) & (int)(gc < ret_chunks)) |
+                       ((int)(gc >= cr_lo) & (int)(gc <= cr_hi)) |
+                       ((int)(gc >= ce_lo) & (int)(gc <= ce_hi)) | (int)(gc == pad_r) |
+                       (int)(gc == pad_e);
+      bits |= (uint32_t)(drop ^ 1) << kc;
+    }
+    return bits;
+  };
 
   // ---- row keys: MFMA B operands, resident for the whole sweep ------------------------
   bf16x8 bfrag[NSUB][C::KSTEPS];
@@ -224,9 +257,6 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
       if (ok) raw = *reinterpret_cast<const uint4*>(kb + (int64_t)i * a.token_stride +
                                                      row_off<D, SPLIT>(t) + half * 8);
       bfrag[s][t] = scale8(raw, g);
-      // Row keys are only ever MFMA operands: keep them in accumulation registers so the
-      // architectural VGPRs stay free for the epilogue (MFMA reads srcB from AGPRs).
-      asm volatile("" : "+a"(bfrag[s][t]));
     }
   }
 
@@ -250,29 +280,62 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
     retired_done = true;
   };
 
+  // ---- LDS addressing ------------------------------------------------------------------
+  // A column's 16-byte piece p is stored in slot p ^ (column & SWZ) of its row, so the 32
+  // lanes that read one piece of 32 consecutive columns hit distinct banks.  Since SWZ < 32,
+  // the swizzle of column c*32 + l32 only depends on l32: the byte offset of k-step t of a
+  // lane's column is a lane constant plus c * (chunk bytes) plus the stage offset.
+  int aoff[C::KSTEPS];
+#pragma unroll
+  for (int t = 0; t < C::KSTEPS; ++t) {
+    const int part = (col_off<D, SPLIT>(t) >> 3) + half;
+    aoff[t] = l32 * (C::DCOL * 2) + ((part ^ (l32 & C::SWZ)) << 4);
+  }
+  const int roff = C::KEY_BYTES + 16 * half;  // this lane's inverse norms inside a chunk
+
+  auto load_rv = [&](const char* st, int c, float (&rv)[16]) {
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const float4 x = *reinterpret_cast<const float4*>(st + roff + c * kChunk * 4 + 32 * g4);
+      rv[4 * g4 + 0] = x.x;
+      rv[4 * g4 + 1] = x.y;
+      rv[4 * g4 + 2] = x.z;
+      rv[4 * g4 + 3] = x.w;
+    }
+  };
+
   // ---- column tiles: global -> LDS by direct (asynchronous) loads, double buffered ------
-  // Each wave moves LOADS_PER_WAVE blocks of 1 KB; lane l of a block lands at byte 16*l.
-  // A column's 16-byte piece p is stored in slot p ^ (column & SWZ) of its row, so the
-  // 32 lanes that read one piece of 32 consecutive columns hit distinct banks.
+  // Each wave moves LOADS_PER_WAVE blocks of 1 KB with buffer loads; lane l of a block lands
+  // at byte 16*l.  Block blk holds columns blk*B .. blk*B+B-1 (B = 64 / PPC), lane l piece
+  // l % PPC of column blk*B + l / PPC, stored in slot piece ^ (column & SWZ).  The buffer
+  // resource of a tile ends at the problem's last column, so the hardware range check turns
+  // loads past it into zeros instead of reads (those columns are never used).
+  constexpr int B = 64 / C::PPC;
+  static_assert((C::SWZ + 1) % B == 0 && ((C::LOADS_PER_WAVE * B) % (C::SWZ + 1)) == 0,
+                "the swizzle of a block's columns must repeat with the block index");
+  const int lcol = lane / C::PPC;
+  int vlane[(C::SWZ + 1) / B];
+#pragma unroll
+  for (int r = 0; r < (C::SWZ + 1) / B; ++r)
+    vlane[r] = lcol * (C::DCOL * 2) + 16 * ((lane % C::PPC) ^ (r * B + lcol));
   int nxt_p = -1;
   float nxt_r = 0.0f;
   auto issue_tile = [&](int tile, int buf) {
     char* st = smem + buf * C::STAGE;
+    const int64_t first = (int64_t)tile * C::TN;
+    const int left = ncols - (int)first;                // > 0 for every issued tile
+    const int nbytes = (left < C::TN ? left : C::TN) * C::DCOL * 2;
 #pragma unroll
     for (int kk = 0; kk < C::LOADS_PER_WAVE; ++kk) {
+      // one resource per 1-KB block, based at the block: the range check sees the whole
+      // offset of every lane
       const int blk = wave * C::LOADS_PER_WAVE + kk;
-      const int e = blk * 64 + lane;
-      const int col = e / C::PPC;
-      const int slot = e - col * C::PPC;
-      const int part = slot ^ (col & C::SWZ);
-      int gcol = tile * C::TN + col;
-      gcol = gcol < ncols ? gcol : 0;            // beyond the last chunk: any valid column
-      __builtin_amdgcn_global_load_lds(
-          (const void*)(pk + (int64_t)gcol * C::DCOL + part * 8),
-          (void __attribute__((address_space(3)))*)(st + blk * 1024), 16, 0, 0);
+      const int rem = nbytes - blk * 1024;
+      load_block_lds(pk + (first * C::DCOL + blk * 512), rem > 0 ? rem : 0,
+                     vlane[kk % ((C::SWZ + 1) / B)], st + blk * 1024);
     }
     if (threadIdx.x < C::TN) {
-      const int col = tile * C::TN + threadIdx.x;
+      const int col = (int)first + threadIdx.x;
       nxt_p = col < ncols ? pc[col] : -1;
       nxt_r = col < ncols ? rc[col] : 0.0f;
     }
@@ -286,98 +349,163 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
 
-  if (ntiles > 0) {
-    issue_tile(0, 0);
-    finish_tile(0);
-  }
-  __syncthreads();
+  // ---- the pending reduction: the last 32-row block of the previous chunk is reduced
+  // while the first MFMA chain of the next chunk runs (software pipelining across chunks).
+  f32x16 pacc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float prv[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) prv[v] = 0.0f;
+  int pgc = 0;
+  uint32_t pmask = 0u;  // result mask of the pending chunk (zero: dropped)
 
-  for (int tile = 0; tile < ntiles; ++tile) {
-    if (tile + 1 < ntiles) issue_tile(tile + 1, (tile + 1) & 1);
-    const char* st = smem + (tile & 1) * C::STAGE;
-    const uint16_t* lk = reinterpret_cast<const uint16_t*>(st);
-    const float* lr = reinterpret_cast<const float*>(st + C::KEY_BYTES);
-    const int* lp = reinterpret_cast<const int*>(st + C::KEY_BYTES + C::TN * 4);
+  auto reduce_into = [&](const f32x16& acc, const float (&rv)[16], int gc, int s, uint32_t m) {
+    const uint32_t best = chunk_best(acc, rv) & m;
+    run_update(best, gc, run[s], cid[s]);
+  };
 
-    // One 32-column chunk: the MFMA chain of 32-row block s runs while the VALU reduces
-    // block s - 1.  RET picks the running maximum, MASKED applies the window / padding test.
-    auto chunk = [&](int c, int gc, auto mask_tag) {
-      constexpr bool MASKED = decltype(mask_tag)::value;
-      const int col = c * kChunk + l32;
-      bf16x8 af[C::KSTEPS];
+  // One tile: each chain's epilogue runs beside the following chain's MFMAs, and the last
+  // chain's epilogue is left pending for the next chunk.  During the last chain, k-step t of
+  // the next chunk's A fragments is read into the registers that MFMA t has just consumed.
+  auto sweep_tile = [&](auto buf_tag, int c0, uint32_t keep) {
+    constexpr int BUF = decltype(buf_tag)::value;
+    const char* st = smem + BUF * C::STAGE;
+    bf16x8 fc[C::KSTEPS];
+#pragma unroll
+    for (int t = 0; t < C::KSTEPS; ++t)
+      fc[t] = *reinterpret_cast<const bf16x8*>(st + aoff[t]);
+#pragma unroll
+    for (int kc = 0; kc < CPT; ++kc) {
+      const int gc = c0 + kc;
+      const uint32_t m = 0u - ((keep >> kc) & 1u);
+      float rcur[16];
+      // with a single row block, chain 0 is also the last chain and carries the prefetch
+      const bool pre0 = (NSUB == 1) && (kc + 1 < CPT);
+      f32x16 x = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < C::KSTEPS; ++t) {
-        const int part = (col_off<D, SPLIT>(t) >> 3) + half;
-        af[t] = *reinterpret_cast<const bf16x8*>(lk + col * C::DCOL + ((part ^ (col & C::SWZ)) << 3));
+        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc[t], bfrag[0][t], x, 0, 0, 0);
+        if (pre0)
+          fc[t] = *reinterpret_cast<const bf16x8*>(st + (kc + 1) * C::CHUNK_BYTES + aoff[t]);
       }
-      float rv[16];
+      reduce_into(pacc, prv, pgc, NSUB - 1, pmask);
+      load_rv(st, kc, rcur);
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const float4 x = *reinterpret_cast<const float4*>(lr + c * kChunk + 8 * g4 + 4 * half);
-        rv[4 * g4 + 0] = x.x;
-        rv[4 * g4 + 1] = x.y;
-        rv[4 * g4 + 2] = x.z;
-        rv[4 * g4 + 3] = x.w;
+      for (int i = 0; i < C::KSTEPS; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+        if (i < 4 || pre0) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedValu, C::VALU_PER_MFMA, 0);
       }
-      auto reduce = [&](const f32x16& acc, int s) {
-        uint32_t best;
-        if constexpr (MASKED) {
-          // column positions read here (rare path) so they are not live across the chunk
-          const int i = wrow0 + s * 32 + l32;
-          best = 0u;
 #pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4) {
-            const int4 jq = *reinterpret_cast<const int4*>(lp + c * kChunk + 8 * g4 + 4 * half);
-            const int jv[4] = {jq.x, jq.y, jq.z, jq.w};
+      for (int s = 1; s < NSUB; ++s) {
+        f32x16 y = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        const bool pre = (s == NSUB - 1) && (kc + 1 < CPT);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int v = 4 * g4 + q;
-              const float y = fmaf(acc[v], rv[v], 3.0f);
-              const uint32_t u = (__float_as_uint(y) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
-              const bool ok = (jv[q] >= 0) && (abs(i - jv[q]) > a.w);
-              best = max(best, ok ? u : 0u);
-            }
-          }
-        } else {
-          best = chunk_best(acc, rv);
+        for (int t = 0; t < C::KSTEPS; ++t) {
+          y = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc[t], bfrag[s][t], y, 0, 0, 0);
+          if (pre)
+            fc[t] = *reinterpret_cast<const bf16x8*>(st + (kc + 1) * C::CHUNK_BYTES + aoff[t]);
         }
-        run_update(best, gc, run[s], cid[s]);
-      };
-      f32x16 prev;
+        reduce_into(x, rcur, gc, s - 1, m);
 #pragma unroll
-      for (int s = 0; s < NSUB; ++s) {
-        f32x16 x = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int t = 0; t < C::KSTEPS; ++t)
-          x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], x, 0, 0, 0);
-        if (s > 0) reduce(prev, s - 1);
-        prev = x;
-        if (s > 0) {
-#pragma unroll
-          for (int i = 0; i < C::KSTEPS; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedValu, C::VALU_PER_MFMA, 0);
-          }
+        for (int i = 0; i < C::KSTEPS; ++i) {
+          __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+          if (pre) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(kSchedValu, C::VALU_PER_MFMA, 0);
         }
+        x = y;
       }
-      reduce(prev, NSUB - 1);
-    };
-
-#pragma unroll 1
-    for (int c = 0; c < CPT; ++c) {
-      const int gc = tile * CPT + c;
-      if (gc >= nchunks) break;
-      if (gc == pm.ret_chunks) retire();
-      const bool masked = (gc >= cr_lo && gc <= cr_hi) || (gc >= ce_lo && gc <= ce_hi) ||
-                          gc == pad_r || gc == pad_e;
-      if (!masked) chunk(c, gc, std::false_type{});
-      else chunk(c, gc, std::true_type{});
+      pacc = x;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) prv[v] = rcur[v];
+      pgc = gc;
+      pmask = m;
     }
-    if (tile + 1 < ntiles) finish_tile((tile + 1) & 1);
-    __syncthreads();
-  }
+  };
 
+  if (ntiles > 0) issue_tile(0, 0);
+#pragma unroll 1
+  for (int tile = 0; tile < ntiles; ++tile) {
+    const int buf = tile & 1;
+    finish_tile(buf);
+    __syncthreads();
+    if (tile + 1 < ntiles) issue_tile(tile + 1, buf ^ 1);
+    const int c0 = tile * CPT;
+    if (c0 == ret_chunks) {            // first evicted chunk: finish and park the S0 results
+      reduce_into(pacc, prv, pgc, NSUB - 1, pmask);
+      pmask = 0u;
+      retire();
+    }
+    const uint32_t keep = __builtin_amdgcn_readfirstlane(keep_bits(c0));
+    if (buf == 0) sweep_tile(std::integral_constant<int, 0>{}, c0, keep);
+    else sweep_tile(std::integral_constant<int, 1>{}, c0, keep);
+  }
+  reduce_into(pacc, prv, pgc, NSUB - 1, pmask);
   if (!retired_done) retire();          // no evicted columns were swept
+
+  // ---- masked pass: the chunks holding window pairs or padding next to real columns, read
+  // straight from the column copy, with the window / padding test per element.  Chunks are
+  // visited out of order here, so equal values keep the smaller chunk index explicitly.
+  auto masked_chunk = [&](int gc, uint32_t (&rs)[NSUB], int (&cs)[NSUB]) {
+    const int col = gc * kChunk + l32;
+    bf16x8 af[C::KSTEPS];
+#pragma unroll
+    for (int t = 0; t < C::KSTEPS; ++t)
+      af[t] = *reinterpret_cast<const bf16x8*>(pk + (int64_t)col * C::DCOL +
+                                               col_off<D, SPLIT>(t) + 8 * half);
+    float rv[16];
+    int jv[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int cc = gc * kChunk + slot_col(v, half);
+      rv[v] = rc[cc];
+      jv[v] = pc[cc];
+    }
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) {
+      f32x16 x = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < C::KSTEPS; ++t)
+        x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], x, 0, 0, 0);
+      const int i = wrow0 + s * 32 + l32;
+      uint32_t best = 0u;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float y = fmaf(x[v], rv[v], 3.0f);
+        const uint32_t u = (__float_as_uint(y) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
+        const bool ok = (jv[v] >= 0) && (abs(i - jv[v]) > a.w);
+        best = max(best, ok ? u : 0u);
+      }
+      const bool upd = (best >> 4) > (rs[s] >> 4) ||
+                       ((best >> 4) == (rs[s] >> 4) && best >= kValidMin && gc < cs[s]);
+      rs[s] = upd ? best : rs[s];
+      cs[s] = upd ? gc : cs[s];
+    }
+  };
+  auto masked_range = [&](int l, int h, uint32_t (&rs)[NSUB], int (&cs)[NSUB]) {
+#pragma unroll 1
+    for (int gc = l; gc <= h; ++gc)
+      if (gc < nchunks) masked_chunk(gc, rs, cs);
+  };
+  // evicted group: the live registers
+  if (a.want_all) {
+    masked_range(ce_lo, ce_hi, run, cid);
+    if (pad_e >= 0 && !(pad_e >= ce_lo && pad_e <= ce_hi)) masked_range(pad_e, pad_e, run, cid);
+  }
+  // S0 group: the parked results
+  {
+    uint32_t rr[NSUB];
+    int rcid[NSUB];
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) {
+      const uint2 v = retired[s * 64 + lane];
+      rr[s] = v.x;
+      rcid[s] = (int)v.y;
+    }
+    masked_range(cr_lo, cr_hi, rr, rcid);
+    if (pad_r >= 0 && !(pad_r >= cr_lo && pad_r <= cr_hi)) masked_range(pad_r, pad_r, rr, rcid);
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) retired[s * 64 + lane] = make_uint2(rr[s], (uint32_t)rcid[s]);
+  }
 
   // ---- resolve: lanes l and l+32 hold the same row over disjoint column halves ----------
 #pragma unroll
@@ -439,7 +567,7 @@ hipError_t run(const SimArgs& a, hipStream_t st) {
 // Tile shapes: (NSUB 32-row blocks per wave, waves per workgroup, 32-column chunks per tile).
 #define TWINKV_CFG_BF16_128 128, false, 3, 4, 4
 #define TWINKV_CFG_BF16_64 64, false, 4, 4, 4
-#define TWINKV_CFG_F32_64 64, true, 2, 4, 4
+#define TWINKV_CFG_F32_64 64, true, 1, 4, 4
 #define TWINKV_CFG_F32_128 128, true, 1, 4, 2
 
 int sim_rows_per_block(int dtype, int d) {

@@ -24,13 +24,16 @@ struct SeqInfo {
 // Per-problem result of the partition step.
 struct ProblemMeta {
   int32_t n_ret;         // |S0|
-  int32_t ret_chunks;    // 32-column chunks holding S0 (last one padded)
+  int32_t ret_chunks;    // 32-column chunks of the S0 group (padded to kGroupAlign columns)
   int32_t total_chunks;  // chunks of S0 followed by chunks of the evicted columns
   int32_t flags;         // bit 0: a key of the problem is non-finite
 };
 
 constexpr int kChunk = 32;           // columns per MFMA chunk (the 32x32x16 tile)
-constexpr int kPermPad = 2 * kChunk; // padding per (head, sequence) in the column lists
+// The S0 group of a column list is padded to a multiple of kGroupAlign columns, so the
+// evicted group starts on a column-tile boundary of the similarity kernel.
+constexpr int kGroupAlign = 128;
+constexpr int kPermPad = kGroupAlign + kChunk;  // padding per (head, sequence) in the column lists
 constexpr int kFlagNonfinite = 1;
 
 // Workspace layout shared by the size query and the launchers.
