@@ -38,8 +38,9 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC>
 struct Cfg {
+  static constexpr int WG_PER_CU = OCC * 4 / NWAVES;  // OCC waves per SIMD
   static constexpr int KSTEPS = SPLIT ? 3 * D / 16 : D / 16;
   static constexpr int DCOL = SPLIT ? 2 * D : D;      // bf16 elements per column in LDS
   static constexpr int PPC = DCOL / 8;                // 16-byte pieces per column
@@ -54,7 +55,8 @@ struct Cfg {
   static constexpr int LOADS_PER_WAVE = TN * PPC / (NWAVES * 64);  // 1-KB direct loads
   static constexpr int VALU_PER_MFMA = (48 + KSTEPS - 1) / KSTEPS;
   static_assert((TN * PPC) % (NWAVES * 64) == 0, "tile copy must divide evenly");
-  static_assert(TN <= NT, "one thread per tile column for the column tables");
+  static_assert(2 * (KEY_BYTES + TN * 8) + RETIRED <= 160 * 1024 / WG_PER_CU,
+                "LDS of WG_PER_CU workgroups must fit one CU");
 };
 
 // Element offset of k-step t inside a column (A operand) / a row (B operand).
@@ -109,12 +111,18 @@ constexpr uint32_t kValidMin = 0x3F800000u;  // packed values >= 1.0f are real c
 // Fourth dword of a raw buffer resource on gfx9-family parts (32-bit data format).
 constexpr int kBufferFlags = 0x00020000;
 
-// 16 bytes per lane from base + voff straight into LDS at lds + 16 * lane, through a raw
-// buffer resource of nbytes: lanes whose offset is past the end read nothing (zeros).
-__device__ inline void load_block_lds(const void* base, int nbytes, int voff, char* lds) {
+// BYTES (4 or 16) per lane from base + voff straight into LDS at lds + BYTES * lane, through
+// a raw buffer resource of nbytes: lanes whose offset is past the end read nothing (zeros).
+__device__ inline void load_block_lds16(const void* base, int nbytes, int voff, char* lds) {
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes, kBufferFlags);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void __attribute__((address_space(3)))*)lds, 16,
+                                           voff, 0, 0, 0);
+}
+__device__ inline void load_block_lds4(const void* base, int nbytes, int voff, char* lds) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes, kBufferFlags);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void __attribute__((address_space(3)))*)lds, 4,
                                            voff, 0, 0, 0);
 }
 
@@ -142,9 +150,9 @@ __device__ inline void run_update(uint32_t best, int gc, uint32_t& run, int& cid
   cid = upd ? gc : cid;
 }
 
-template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
-__global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
-  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT>;
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC>
+__global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kernel(SimArgs a) {
+  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC>;
   static_assert(kGroupAlign % C::TN == 0, "the evicted group must start on a tile boundary");
   __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE + C::RETIRED];
 
@@ -318,8 +326,6 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
 #pragma unroll
   for (int r = 0; r < (C::SWZ + 1) / B; ++r)
     vlane[r] = lcol * (C::DCOL * 2) + 16 * ((lane % C::PPC) ^ (r * B + lcol));
-  int nxt_p = -1;
-  float nxt_r = 0.0f;
   auto issue_tile = [&](int tile, int buf) {
     char* st = smem + buf * C::STAGE;
     const int64_t first = (int64_t)tile * C::TN;
@@ -331,21 +337,21 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
       // offset of every lane
       const int blk = wave * C::LOADS_PER_WAVE + kk;
       const int rem = nbytes - blk * 1024;
-      load_block_lds(pk + (first * C::DCOL + blk * 512), rem > 0 ? rem : 0,
-                     vlane[kk % ((C::SWZ + 1) / B)], st + blk * 1024);
+      load_block_lds16(pk + (first * C::DCOL + blk * 512), rem > 0 ? rem : 0,
+                       vlane[kk % ((C::SWZ + 1) / B)], st + blk * 1024);
     }
-    if (threadIdx.x < C::TN) {
-      const int col = (int)first + threadIdx.x;
-      nxt_p = col < ncols ? pc[col] : -1;
-      nxt_r = col < ncols ? rc[col] : 0.0f;
+    // The column tables (inverse norms, then positions) in 256-byte pieces, 4 bytes a lane.
+    const int tbytes = (left < C::TN ? left : C::TN) * 4;
+#pragma unroll
+    for (int pc4 = wave; pc4 < C::TN / 32; pc4 += NWAVES) {
+      const int part = pc4 % (C::TN / 64);
+      const int rem = tbytes - part * 256;
+      const void* src = pc4 < C::TN / 64 ? (const void*)(rc + first + part * 64)
+                                          : (const void*)(pc + first + part * 64);
+      load_block_lds4(src, rem > 0 ? rem : 0, 4 * lane, st + C::KEY_BYTES + pc4 * 256);
     }
   };
-  auto finish_tile = [&](int buf) {  // column tables of the issued tile, then wait for all
-    char* st = smem + buf * C::STAGE;
-    if (threadIdx.x < C::TN) {
-      reinterpret_cast<float*>(st + C::KEY_BYTES)[threadIdx.x] = nxt_r;
-      reinterpret_cast<int*>(st + C::KEY_BYTES + C::TN * 4)[threadIdx.x] = nxt_p;
-    }
+  auto finish_tile = [&]() {  // wait for this wave's direct loads of the issued tile
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
 
@@ -426,12 +432,17 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
 #pragma unroll 1
   for (int tile = 0; tile < ntiles; ++tile) {
     const int buf = tile & 1;
-    finish_tile(buf);
+    finish_tile();
     __syncthreads();
     if (tile + 1 < ntiles) issue_tile(tile + 1, buf ^ 1);
     const int c0 = tile * CPT;
-    if (c0 == ret_chunks) {            // first evicted chunk: finish and park the S0 results
-      reduce_into(pacc, prv, pgc, NSUB - 1, pmask);
+    if (c0 == ret_chunks) {
+      // First evicted chunk: finish the pending S0 reduction here and park the S0 results.
+      // The opaque copy keeps the compiler from moving the tile body's own pending
+      // reduction out of the body to share it with this rare path.
+      f32x16 pa = pacc;
+      asm volatile("" : "+v"(pa));
+      reduce_into(pa, prv, pgc, NSUB - 1, pmask);
       pmask = 0u;
       retire();
     }
@@ -551,24 +562,33 @@ __global__ __launch_bounds__(NWAVES * 64, 2) void sim_reduce_kernel(SimArgs a) {
   }
 }
 
-template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT>
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC>
 hipError_t run(const SimArgs& a, hipStream_t st) {
-  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT>;
+  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC>;
   const int64_t groups = a.n_heads >= 8 ? 8LL * ((a.n_heads + 7) / 8) : (int64_t)a.n_heads;
   const int64_t blocks = groups * a.total_tiles;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC>), dim3((unsigned)blocks),
                      dim3(C::NT), 0, st, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Tile shapes: (NSUB 32-row blocks per wave, waves per workgroup, 32-column chunks per tile).
-#define TWINKV_CFG_BF16_128 128, false, 3, 4, 4
-#define TWINKV_CFG_BF16_64 64, false, 4, 4, 4
-#define TWINKV_CFG_F32_64 64, true, 1, 4, 4
-#define TWINKV_CFG_F32_128 128, true, 1, 4, 2
+// Tile shapes: (d, fp32 split, NSUB 32-row blocks per wave, waves per workgroup, 32-column
+// chunks per LDS tile, waves per SIMD).  Overridable at build time for tuning sweeps.
+#ifndef TWINKV_CFG_BF16_128
+#define TWINKV_CFG_BF16_128 128, false, 3, 4, 4, 2
+#endif
+#ifndef TWINKV_CFG_BF16_64
+#define TWINKV_CFG_BF16_64 64, false, 4, 4, 4, 2
+#endif
+#ifndef TWINKV_CFG_F32_64
+#define TWINKV_CFG_F32_64 64, true, 1, 4, 4, 2
+#endif
+#ifndef TWINKV_CFG_F32_128
+#define TWINKV_CFG_F32_128 128, true, 1, 4, 2, 2
+#endif
 
 int sim_rows_per_block(int dtype, int d) {
   if (dtype == 0 && d == 128) return Cfg<TWINKV_CFG_BF16_128>::RB;

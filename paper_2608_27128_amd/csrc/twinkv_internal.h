@@ -32,7 +32,10 @@ struct ProblemMeta {
 constexpr int kChunk = 32;           // columns per MFMA chunk (the 32x32x16 tile)
 // The S0 group of a column list is padded to a multiple of kGroupAlign columns, so the
 // evicted group starts on a column-tile boundary of the similarity kernel.
-constexpr int kGroupAlign = 128;
+#ifndef TWINKV_GROUP_ALIGN
+#define TWINKV_GROUP_ALIGN 128
+#endif
+constexpr int kGroupAlign = TWINKV_GROUP_ALIGN;
 constexpr int kPermPad = kGroupAlign + kChunk;  // padding per (head, sequence) in the column lists
 constexpr int kFlagNonfinite = 1;
 
