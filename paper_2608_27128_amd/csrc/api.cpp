@@ -1,6 +1,6 @@
 // Host layer of the C ABI declared in include/twinkv.h: argument validation (pure host code,
 // done before anything is enqueued), workspace layout, the per-sequence schedule table and
-// the kernel launches (K1a normalise, K1b partition, K2 similarity, K3 repair).
+// the kernel launches (K1a partition, K1b key preparation, K2 similarity, K3 repair).
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -157,10 +157,14 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
   uint16_t* hilo = dtype == TWINKV_F32 ? reinterpret_cast<uint16_t*>(ws + L.hilo) : nullptr;
   uint16_t* pkeys = reinterpret_cast<uint16_t*>(ws + L.pkeys);
 
-  int e = launch_normalise(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, rinv, hilo, stream);
+  int e = launch_partition(retained, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT, pcol, rcol, prank,
+                           pmeta, status, stream);
   if (e) return hip_status(e);
-  e = launch_partition(retained, rinv, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT, pcol, rcol, prank,
-                       pmeta, status, stream);
+  int max_len = 0;
+  for (int s = 0; s < bt.n_seqs; ++s) max_len = std::max(max_len, (int)(cu[s + 1] - cu[s]));
+  e = launch_prepare_keys(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, bt.PT,
+                          max_len, retained, prank, pmeta, dtab, bt.n_seqs, rinv, rcol, hilo, pkeys, status,
+                          stream);
   if (e) return hip_status(e);
 
   SimArgs a;
@@ -173,13 +177,6 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
     a.head_stride = head_stride;
     a.token_stride = token_stride;
   }
-  int max_len = 0;
-  for (int s = 0; s < bt.n_seqs; ++s) max_len = std::max(max_len, (int)(cu[s + 1] - cu[s]));
-  const int dcol = dtype == TWINKV_F32 ? 2 * d : d;
-  e = launch_gather_columns(reinterpret_cast<const uint16_t*>(a.keys), a.head_stride, a.token_stride,
-                            dcol, pcol, pmeta, dtab, bt.n_heads, bt.n_seqs, max_len, bt.PT, pkeys,
-                            stream);
-  if (e) return hip_status(e);
   a.rinv = rinv;
   a.pkeys = pkeys;
   a.pcol = pcol;

@@ -1,11 +1,13 @@
-// K1a: per-key inverse l2 norm (Sec. 3.2: k_hat = k / ||k||_2) and, for fp32 keys, the bf16
-//      hi/lo split the similarity kernel multiplies on bf16 MFMA.
-// K1b: per-problem stable partition of the positions into [S0 | evicted] column lists (the
+// K1a: per-problem stable partition of the positions into [S0 | evicted] column lists (the
 //      S0 list padded to a multiple of kGroupAlign columns, the evicted list to whole
-//      32-column chunks), carrying the inverse norm of every column.
+//      32-column chunks), from the retained mask alone.
+// K1b: one pass over the keys: per-key inverse l2 norm (Sec. 3.2: k_hat = k / ||k||_2), and
+//      the key itself copied to its slot of the partitioned column list (bf16; for fp32 keys
+//      the bf16 hi/lo split the similarity kernel multiplies on bf16 MFMA, which also goes
+//      to a row-ordered plane for the kernel's row operands).
 //
-// Both kernels are HBM-bound streams: K1a reads d*esize bytes and writes 4 bytes per key
-// (+ 4d bytes of planes for fp32 keys); K1b reads 1 + 4 bytes and writes 8 bytes per key.
+// K1a reads 1 byte and writes 8 bytes per key.  K1b is an HBM stream: it reads d*esize bytes
+// (+5 bytes of mask and rank) and writes d*2 (+4d for fp32) + 8 bytes per key.
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"
@@ -20,64 +22,6 @@ __device__ inline uint16_t bf16_rne(float f) {
 }
 
 __device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
-// LPT lanes cooperate on one key; each lane owns 16 contiguous bytes of it.
-template <int D, bool F32>
-__global__ __launch_bounds__(256) void normalise_kernel(const uint8_t* __restrict__ keys,
-                                                        int64_t n_tok, int64_t T, int64_t hs_bytes,
-                                                        int64_t ts_bytes, float* __restrict__ rinv,
-                                                        uint16_t* __restrict__ hilo) {
-  constexpr int ESZ = F32 ? 4 : 2;
-  constexpr int LPT = D * ESZ / 16;
-  constexpr int TPB = 256 / LPT;
-  static_assert(LPT <= 64 && (64 % LPT) == 0, "a key must fit inside one wave");
-  const int sub = threadIdx.x % LPT;
-  const int64_t tok = (int64_t)blockIdx.x * TPB + threadIdx.x / LPT;
-  const bool valid = tok < n_tok;
-  const int64_t h = valid ? tok / T : 0;
-  const int64_t t = valid ? tok - h * T : 0;
-  uint4 raw = make_uint4(0, 0, 0, 0);
-  if (valid) raw = *reinterpret_cast<const uint4*>(keys + h * hs_bytes + t * ts_bytes + sub * 16);
-  double ss = 0.0;
-  if constexpr (F32) {
-    float v[4] = {__uint_as_float(raw.x), __uint_as_float(raw.y), __uint_as_float(raw.z),
-                  __uint_as_float(raw.w)};
-    uint16_t hi[4], lo[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      ss += (double)v[e] * (double)v[e];
-      hi[e] = bf16_rne(v[e]);
-      lo[e] = bf16_rne(v[e] - bf16_to_f32(hi[e]));  // v - hi is exact in fp32
-    }
-    if (valid) {
-      uint16_t* dst = hilo + tok * (2 * D) + sub * 4;
-      uint2 phi, plo;
-      phi.x = hi[0] | ((uint32_t)hi[1] << 16);
-      phi.y = hi[2] | ((uint32_t)hi[3] << 16);
-      plo.x = lo[0] | ((uint32_t)lo[1] << 16);
-      plo.y = lo[2] | ((uint32_t)lo[3] << 16);
-      *reinterpret_cast<uint2*>(dst) = phi;
-      *reinterpret_cast<uint2*>(dst + D) = plo;
-    }
-  } else {
-    const uint32_t wds[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const double a = (double)__uint_as_float(wds[e] << 16);
-      const double b = (double)__uint_as_float(wds[e] & 0xFFFF0000u);
-      ss += a * a + b * b;
-    }
-  }
-#pragma unroll
-  for (int off = LPT / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, LPT);
-  if (valid && sub == 0) {
-    float r;
-    if (!(ss < 1.0e300)) r = __uint_as_float(0x7FC00000u);  // NaN / Inf key: marker for K1b
-    else if (ss > 0.0) r = (float)(1.0 / sqrt(ss));
-    else r = 0.0f;                                        // zero key: similarity 0 to all
-    rinv[tok] = r;
-  }
-}
 
 template <int NT>
 __device__ inline int block_sum(int v, int* s_red) {
@@ -95,11 +39,11 @@ __device__ inline int block_sum(int v, int* s_red) {
 
 constexpr int kPartThreads = 256;
 
+// One workgroup per (head, sequence) problem.
 __global__ __launch_bounds__(kPartThreads) void partition_kernel(
-    const uint8_t* __restrict__ retained, const float* __restrict__ rinv,
-    const SeqInfo* __restrict__ seqtab, int n_seqs, int64_t T, int64_t PT,
-    int32_t* __restrict__ pcol, float* __restrict__ rcol, int32_t* __restrict__ prank,
-    ProblemMeta* __restrict__ pmeta, int32_t* __restrict__ status) {
+    const uint8_t* __restrict__ retained, const SeqInfo* __restrict__ seqtab, int n_seqs,
+    int64_t T, int64_t PT, int32_t* __restrict__ pcol, float* __restrict__ rcol,
+    int32_t* __restrict__ prank, ProblemMeta* __restrict__ pmeta, int32_t* __restrict__ status) {
   __shared__ int s_red[kPartThreads / 64];
   __shared__ int s_wave[kPartThreads / 64];
   const int q = blockIdx.x;
@@ -108,18 +52,14 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
   const SeqInfo si = seqtab[s];
   const int len = si.len;
   const uint8_t* ret = retained ? retained + h * T + si.start : nullptr;
-  const float* rv = rinv + h * T + si.start;
   int32_t* pc = pcol + h * PT + si.perm_off;
   float* rc = rcol + h * PT + si.perm_off;
   int32_t* pr = prank + h * PT + si.perm_off;
 
-  int cnt = 0, bad = 0;
-  for (int t = threadIdx.x; t < len; t += kPartThreads) {
-    cnt += (ret != nullptr && ret[t] != 0);
-    bad |= !(fabsf(rv[t]) <= 3.4e38f);
-  }
+  int cnt = 0;
+  if (ret != nullptr)
+    for (int t = threadIdx.x; t < len; t += kPartThreads) cnt += (ret[t] != 0);
   const int n_ret = block_sum<kPartThreads>(cnt, s_red);
-  const int any_bad = block_sum<kPartThreads>(bad, s_red);
   const int ret_pad = (n_ret + kGroupAlign - 1) / kGroupAlign * kGroupAlign;
   const int n_ev = len - n_ret;
   const int ev_pad = (n_ev + kChunk - 1) / kChunk * kChunk;
@@ -144,14 +84,13 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
     }
     if (in) {
       const int ret_before = ret_before_round + wbase + pre;
-      const int p = r ? ret_before : ret_pad + (t - ret_before);
-      pc[p] = t;
-      rc[p] = rv[t];
+      pc[r ? ret_before : ret_pad + (t - ret_before)] = t;
       pr[t] = ret_before;
     }
     ret_before_round += tot;
     __syncthreads();
   }
+  // padding columns: no position, inverse norm 0 (their keys are never used)
   for (int k = n_ret + (int)threadIdx.x; k < ret_pad; k += kPartThreads) {
     pc[k] = -1;
     rc[k] = 0.0f;
@@ -166,87 +105,151 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
     m.n_ret = n_ret;
     m.ret_chunks = ret_pad / kChunk;
     m.total_chunks = (ret_pad + ev_pad) / kChunk;
-    m.flags = any_bad ? kFlagNonfinite : 0;
+    m.flags = 0;
     pmeta[q] = m;
-    if (status) status[q] = any_bad ? 2 /* TWINKV_PROBLEM_NONFINITE */ : 0;
+    if (status) status[q] = 0;
   }
 }
 
-// K1c: one 16-byte piece per thread; blockIdx.y = problem, blockIdx.x = group of columns.
-constexpr int kGatherThreads = 256;
-
-__global__ __launch_bounds__(kGatherThreads) void gather_columns_kernel(
-    const uint16_t* __restrict__ src, int64_t src_hs, int64_t src_ts, int dcol,
-    const int32_t* __restrict__ pcol, const ProblemMeta* __restrict__ pmeta,
-    const SeqInfo* __restrict__ seqtab, int n_seqs, int64_t PT, uint16_t* __restrict__ pkeys) {
-  const int q = blockIdx.y;
-  const int h = q / n_seqs;
-  const int s = q - h * n_seqs;
-  const SeqInfo si = seqtab[s];
-  const int ncols = pmeta[q].total_chunks * kChunk;
-  const int pieces = dcol / 8;                      // 16-byte pieces per column
-  const int cols_per_block = kGatherThreads / pieces;
-  const int c = blockIdx.x * cols_per_block + threadIdx.x / pieces;
-  const int part = threadIdx.x % pieces;
-  if (c >= ncols) return;
-  const int64_t p = h * PT + si.perm_off + c;
-  const int j = pcol[p];
-  uint4 v = make_uint4(0, 0, 0, 0);
-  if (j >= 0) v = *reinterpret_cast<const uint4*>(src + h * src_hs + (int64_t)(si.start + j) * src_ts + part * 8);
-  *reinterpret_cast<uint4*>(pkeys + p * dcol + part * 8) = v;
-}
-
+// LPT lanes cooperate on one key; each lane owns 16 contiguous bytes of it.  blockIdx.y is
+// the (head, sequence) problem, blockIdx.x a group of TPB of its tokens, so the problem's
+// table entries are uniform across the workgroup.
 template <int D, bool F32>
-hipError_t run_normalise(const void* keys, int n_heads, int64_t T, int64_t hs, int64_t ts,
-                         float* rinv, uint16_t* hilo, hipStream_t st) {
+__global__ __launch_bounds__(256) void prepare_keys_kernel(
+    const uint8_t* __restrict__ keys, int64_t T, int64_t hs_bytes, int64_t ts_bytes, int64_t PT,
+    const uint8_t* __restrict__ retained, const int32_t* __restrict__ prank,
+    ProblemMeta* __restrict__ pmeta, const SeqInfo* __restrict__ seqtab, int n_seqs,
+    float* __restrict__ rinv, float* __restrict__ rcol, uint16_t* __restrict__ hilo,
+    uint16_t* __restrict__ pkeys, int32_t* __restrict__ status, int q0) {
   constexpr int ESZ = F32 ? 4 : 2;
   constexpr int LPT = D * ESZ / 16;
   constexpr int TPB = 256 / LPT;
-  const int64_t n_tok = (int64_t)n_heads * T;
-  if (n_tok == 0) return hipSuccess;
-  const int64_t blocks = (n_tok + TPB - 1) / TPB;
-  hipLaunchKernelGGL((normalise_kernel<D, F32>), dim3((unsigned)blocks), dim3(256), 0, st,
-                     (const uint8_t*)keys, n_tok, T, hs * ESZ, ts * ESZ, rinv, hilo);
-  return hipGetLastError();
+  constexpr int DCOL = F32 ? 2 * D : D;
+  static_assert(LPT <= 64 && (64 % LPT) == 0, "a key must fit inside one wave");
+  const int q = q0 + (int)blockIdx.y;
+  const int64_t h = q / n_seqs;
+  const int s = q - (int)h * n_seqs;
+  const SeqInfo si = seqtab[s];
+  const int tl0 = blockIdx.x * TPB;
+  if (tl0 >= si.len) return;                 // sequences shorter than the longest
+  const int sub = threadIdx.x % LPT;
+  const int tl = tl0 + threadIdx.x / LPT;
+  const bool valid = tl < si.len;
+  const int64_t tt = si.start + (valid ? tl : 0);
+  const int64_t base = h * PT + si.perm_off;
+  uint4 raw = make_uint4(0, 0, 0, 0);
+  if (valid) raw = *reinterpret_cast<const uint4*>(keys + h * hs_bytes + tt * ts_bytes + sub * 16);
+  const bool r = retained != nullptr && retained[h * T + tt] != 0;
+  const int pr = prank[base + (valid ? tl : 0)];
+  const int p = r ? pr : pmeta[q].ret_chunks * kChunk + ((valid ? tl : 0) - pr);
+  uint16_t* dst = pkeys + (base + p) * DCOL;
+
+  double ss = 0.0;
+  if constexpr (F32) {
+    float v[4] = {__uint_as_float(raw.x), __uint_as_float(raw.y), __uint_as_float(raw.z),
+                  __uint_as_float(raw.w)};
+    uint16_t hs[4], ls[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      ss += (double)v[e] * (double)v[e];
+      hs[e] = bf16_rne(v[e]);
+      ls[e] = bf16_rne(v[e] - bf16_to_f32(hs[e]));  // v - hi is exact in fp32
+    }
+    if (valid) {
+      uint2 phi, plo;
+      phi.x = hs[0] | ((uint32_t)hs[1] << 16);
+      phi.y = hs[2] | ((uint32_t)hs[3] << 16);
+      plo.x = ls[0] | ((uint32_t)ls[1] << 16);
+      plo.y = ls[2] | ((uint32_t)ls[3] << 16);
+      uint16_t* row = hilo + (h * T + tt) * (2 * D) + sub * 4;
+      *reinterpret_cast<uint2*>(row) = phi;
+      *reinterpret_cast<uint2*>(row + D) = plo;
+      *reinterpret_cast<uint2*>(dst + sub * 4) = phi;
+      *reinterpret_cast<uint2*>(dst + D + sub * 4) = plo;
+    }
+  } else {
+    const uint32_t wds[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double x0 = (double)__uint_as_float(wds[e] << 16);
+      const double x1 = (double)__uint_as_float(wds[e] & 0xFFFF0000u);
+      ss += x0 * x0 + x1 * x1;
+    }
+    if (valid) *reinterpret_cast<uint4*>(dst + sub * 8) = raw;
+  }
+#pragma unroll
+  for (int off = LPT / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, LPT);
+  if (valid && sub == 0) {
+    float rv;
+    const bool bad = !(ss < 1.0e300);                    // NaN or Inf in the key
+    if (bad) rv = __uint_as_float(0x7FC00000u);
+    else if (ss > 0.0) rv = (float)(1.0 / sqrt(ss));
+    else rv = 0.0f;                                       // zero key: similarity 0 to all
+    rinv[h * T + tt] = rv;
+    rcol[base + p] = rv;
+    if (bad) {
+      atomicOr(&pmeta[q].flags, kFlagNonfinite);
+      if (status) status[q] = 2;  // TWINKV_PROBLEM_NONFINITE
+    }
+  }
+}
+
+template <int D, bool F32>
+hipError_t run_prepare(const void* keys, int n_heads, int64_t T, int64_t hs, int64_t ts,
+                       int64_t PT, int max_len, const uint8_t* retained, const int32_t* prank,
+                       ProblemMeta* pmeta, const SeqInfo* seqtab, int n_seqs, float* rinv,
+                       float* rcol, uint16_t* hilo, uint16_t* pkeys, int32_t* status,
+                       hipStream_t st) {
+  constexpr int ESZ = F32 ? 4 : 2;
+  constexpr int LPT = D * ESZ / 16;
+  constexpr int TPB = 256 / LPT;
+  if (max_len == 0 || n_heads == 0) return hipSuccess;
+  const int64_t bx = (max_len + TPB - 1) / TPB;
+  const int64_t P = (int64_t)n_heads * n_seqs;
+  for (int64_t q0 = 0; q0 < P; q0 += 65535) {  // problems along y, in slices the grid holds
+    const int64_t by = P - q0 < 65535 ? P - q0 : 65535;
+    hipLaunchKernelGGL((prepare_keys_kernel<D, F32>), dim3((unsigned)bx, (unsigned)by),
+                       dim3(256), 0, st, (const uint8_t*)keys, T, hs * ESZ, ts * ESZ, PT,
+                       retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status,
+                       (int)q0);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace
 
-int launch_normalise(const void* keys, int dtype, int d, int n_heads, int64_t T,
-                     int64_t head_stride, int64_t token_stride, float* rinv, uint16_t* hilo,
-                     void* stream) {
-  hipStream_t st = (hipStream_t)stream;
-  if (dtype == 0 && d == 64) return run_normalise<64, false>(keys, n_heads, T, head_stride, token_stride, rinv, hilo, st);
-  if (dtype == 0 && d == 128) return run_normalise<128, false>(keys, n_heads, T, head_stride, token_stride, rinv, hilo, st);
-  if (dtype == 1 && d == 64) return run_normalise<64, true>(keys, n_heads, T, head_stride, token_stride, rinv, hilo, st);
-  if (dtype == 1 && d == 128) return run_normalise<128, true>(keys, n_heads, T, head_stride, token_stride, rinv, hilo, st);
-  return hipErrorInvalidValue;
-}
-
-int launch_partition(const uint8_t* retained, const float* rinv, const SeqInfo* seqtab,
-                     int n_heads, int n_seqs, int64_t T, int64_t PT, int32_t* pcol, float* rcol,
-                     int32_t* prank, ProblemMeta* pmeta, int32_t* status, void* stream) {
+int launch_partition(const uint8_t* retained, const SeqInfo* seqtab, int n_heads, int n_seqs,
+                     int64_t T, int64_t PT, int32_t* pcol, float* rcol, int32_t* prank,
+                     ProblemMeta* pmeta, int32_t* status, void* stream) {
   const int64_t P = (int64_t)n_heads * n_seqs;
   if (P == 0) return hipSuccess;
   hipLaunchKernelGGL(partition_kernel, dim3((unsigned)P), dim3(kPartThreads), 0,
-                     (hipStream_t)stream, retained, rinv, seqtab, n_seqs, T, PT, pcol, rcol,
-                     prank, pmeta, status);
+                     (hipStream_t)stream, retained, seqtab, n_seqs, T, PT, pcol, rcol, prank,
+                     pmeta, status);
   return hipGetLastError();
 }
 
-int launch_gather_columns(const uint16_t* src, int64_t src_head_stride, int64_t src_token_stride,
-                          int dcol, const int32_t* pcol, const ProblemMeta* pmeta,
-                          const SeqInfo* seqtab, int n_heads, int n_seqs, int max_len, int64_t PT,
-                          uint16_t* pkeys, void* stream) {
-  const int64_t P = (int64_t)n_heads * n_seqs;
-  if (P == 0 || max_len == 0) return hipSuccess;
-  const int cols_per_block = kGatherThreads / (dcol / 8);
-  const int max_cols = max_len + kPermPad;
-  const unsigned gx = (unsigned)((max_cols + cols_per_block - 1) / cols_per_block);
-  hipLaunchKernelGGL(gather_columns_kernel, dim3(gx, (unsigned)P), dim3(kGatherThreads), 0,
-                     (hipStream_t)stream, src, src_head_stride, src_token_stride, dcol, pcol, pmeta,
-                     seqtab, n_seqs, PT, pkeys);
-  return hipGetLastError();
+int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t T,
+                        int64_t head_stride, int64_t token_stride, int64_t PT, int max_len,
+                        const uint8_t* retained, const int32_t* prank, ProblemMeta* pmeta,
+                        const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
+                        uint16_t* hilo, uint16_t* pkeys, int32_t* status, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == 0 && d == 64)
+    return run_prepare<64, false>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
+                                  prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+  if (dtype == 0 && d == 128)
+    return run_prepare<128, false>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
+                                   prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+  if (dtype == 1 && d == 64)
+    return run_prepare<64, true>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
+                                 prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+  if (dtype == 1 && d == 128)
+    return run_prepare<128, true>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
+                                  prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace twinkv

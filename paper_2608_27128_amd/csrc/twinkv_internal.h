@@ -49,25 +49,22 @@ struct Layout {
 // ---- launchers (defined in the kernel translation units) ----
 // Each returns 0 on success or a hipError_t value.
 
-// K1a: inverse l2 norm of every key (fp64 accumulation) and, for fp32 keys, the bf16
-// hi/lo planes [n_heads][T][2d] the similarity kernel multiplies.
-int launch_normalise(const void* keys, int dtype, int d, int n_heads, int64_t T,
-                     int64_t head_stride, int64_t token_stride, float* rinv, uint16_t* hilo,
-                     void* stream);
+// K1a: stable partition of each problem's positions into [S0 | evicted] column lists from the
+// retained mask: pcol (positions, -1 for padding), prank[t] = number of S0 positions before t
+// (t = 0..len), the per-problem meta, rcol = 0 at padding, status = 0.
+int launch_partition(const uint8_t* retained, const SeqInfo* seqtab, int n_heads, int n_seqs,
+                     int64_t T, int64_t PT, int32_t* pcol, float* rcol, int32_t* prank,
+                     ProblemMeta* pmeta, int32_t* status, void* stream);
 
-// K1b: stable partition of each problem's positions into [S0 | evicted] column lists,
-// padded to whole chunks, with the inverse norm of every listed column, and
-// prank[t] = number of S0 positions before t (t = 0..len) per problem.
-int launch_partition(const uint8_t* retained, const float* rinv, const SeqInfo* seqtab,
-                     int n_heads, int n_seqs, int64_t T, int64_t PT, int32_t* pcol, float* rcol,
-                     int32_t* prank, ProblemMeta* pmeta, int32_t* status, void* stream);
-
-// K1c: copy of the column keys in partitioned order, pkeys[h][PT][dcol] (bf16; padding zero).
-// src/src_head_stride/src_token_stride in uint16 elements; dcol = d (bf16) or 2d (hi/lo).
-int launch_gather_columns(const uint16_t* src, int64_t src_head_stride, int64_t src_token_stride,
-                          int dcol, const int32_t* pcol, const ProblemMeta* pmeta,
-                          const SeqInfo* seqtab, int n_heads, int n_seqs, int max_len, int64_t PT,
-                          uint16_t* pkeys, void* stream);
+// K1b: one pass over the keys after K1a: inverse l2 norm of every key (fp64 accumulation) to
+// rinv and to rcol at the key's column slot, the key copied to pkeys[h][PT][dcol] at that slot
+// (bf16; dcol = 2d bf16 hi/lo for fp32 keys, which also go to the row plane hilo
+// [n_heads][T][2d]); a non-finite key sets the problem's flag and status.
+int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t T,
+                        int64_t head_stride, int64_t token_stride, int64_t PT, int max_len,
+                        const uint8_t* retained, const int32_t* prank, ProblemMeta* pmeta,
+                        const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
+                        uint16_t* hilo, uint16_t* pkeys, int32_t* status, void* stream);
 
 struct SimArgs {
   const void* keys;          // bf16 keys, or the hi/lo planes for fp32 keys
