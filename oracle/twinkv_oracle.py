@@ -10,6 +10,10 @@ for KV Cache Eviction via Pairwise Key Redundancy"):
                          -1 when no such key exists
   * Sec. 3.4             orphans / redundant donors, severity ranking, m = min(|O|,|D|),
                          the budget-preserving swap producing S1 with |S1| = |S0|
+  * Sec. 3.2, Eq. 2-3    the standalone scorer: twin counts r_i, scores s_i = -r_i / n,
+                         and the retained set of the highest scores with the sink and
+                         recent regions at the maximum score
+  * Sec. 2 (Fig. 1b)     prevalence: how many tokens have at least one twin, per threshold
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library:
@@ -26,6 +30,10 @@ Readings where the paper is silent (each is exercised by a pin test):
       ascending; donors: b descending then index ascending).
   R11 the swap is one simultaneous pass against S0; b is not recomputed between swaps.
   R16 w >= 0, which makes the paper's extra j != i condition implied by |i-j| > w.
+  R19 the scorer's budget K is given directly (the paper's ceil((1-rho) n) is the caller's);
+      among equal scores the later position is retained first (recency).
+  R20 the protected regions take the maximum score, so with K >= |P| they are all kept;
+      with K < |P| the same order (later position first) decides among them.
 Indices are 0-based positions within a sequence (the paper's 1-based positions only
 enter through |i-j| and region sizes, which the shift does not change).
 
@@ -39,7 +47,8 @@ import numpy as np
 __all__ = [
     "decode_keys", "normalise", "similarity_rows", "window_domain", "best_twin",
     "nn_scores", "classify", "rank_severity", "repair", "repair_problem",
-    "protected_mask",
+    "protected_mask", "twin_counts", "redundancy_scores", "evict_by_score",
+    "score_evict_problem", "prevalence",
 ]
 
 # Rows of the similarity matrix are evaluated in independent groups so that an
@@ -207,3 +216,77 @@ def repair_problem(keys: np.ndarray, dtype: str, s0: np.ndarray, budget: int, ta
     out = repair(sc["best_ret"], s0, tau, n_sink, n_recent)
     out.update(sc)
     return out
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.2, Eq. 2-3: the standalone scorer
+# ----------------------------------------------------------------------------
+def twin_counts(keys: np.ndarray, dtype: str, tau: float, w: int,
+                rows: np.ndarray | None = None, margin: float = 0.0) -> dict:
+    """Eq. 2: r_i = #{ j : |i - j| > w, sim(i, j) > tau } for the requested rows.
+
+    With margin > 0, also the counts at tau + margin and tau - margin: bounds on what a
+    computation whose similarities are within margin of these can report.
+    """
+    if w < 0:
+        raise ValueError("w must be >= 0")
+    K = decode_keys(keys, dtype)
+    n = K.shape[0]
+    Khat = normalise(K)
+    rows = np.arange(n) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = {"counts": np.zeros(len(rows), dtype=np.int64)}
+    if margin > 0:
+        out["counts_lo"] = np.zeros(len(rows), dtype=np.int64)
+        out["counts_hi"] = np.zeros(len(rows), dtype=np.int64)
+    step = max(1, _SLAB_ELEMS // max(n, 1))
+    for a in range(0, len(rows), step):
+        r = rows[a:a + step]
+        S = similarity_rows(Khat, r)
+        valid = window_domain(r, n, w)
+        out["counts"][a:a + step] = np.sum(valid & (S > tau), axis=1)
+        if margin > 0:
+            out["counts_lo"][a:a + step] = np.sum(valid & (S > tau + margin), axis=1)
+            out["counts_hi"][a:a + step] = np.sum(valid & (S > tau - margin), axis=1)
+    return out
+
+
+def redundancy_scores(counts: np.ndarray, n: int) -> np.ndarray:
+    """Eq. 3: s_i = -r_i / n (fewer twins, higher score)."""
+    return -np.asarray(counts, dtype=np.float64) / float(n)
+
+
+def evict_by_score(counts: np.ndarray, budget: int, n_sink: int, n_recent: int) -> np.ndarray:
+    """The retained set of Sec. 3.2: the `budget` highest scores, the sink and recent
+    regions at the maximum score (R20), equal scores resolved toward the later position
+    (R19).  Returns a uint8 mask."""
+    counts = np.asarray(counts, dtype=np.int64)
+    n = len(counts)
+    if budget < 0:
+        raise ValueError("budget must be >= 0")
+    score = np.where(protected_mask(n, n_sink, n_recent), np.inf, redundancy_scores(counts, n))
+    pos = np.arange(n)
+    order = np.lexsort((-pos, -score))     # score descending, then position descending
+    keep = np.zeros(n, dtype=np.uint8)
+    keep[order[:min(budget, n)]] = 1
+    return keep
+
+
+def score_evict_problem(keys: np.ndarray, dtype: str, budget: int, tau: float, w: int,
+                        n_sink: int, n_recent: int) -> dict:
+    """The scorer of Sec. 3.2 on one (sequence, layer, KV head) problem: Eq. 2 counts,
+    Eq. 3 scores and the retained set."""
+    c = twin_counts(keys, dtype, tau, w)["counts"]
+    n = len(c)
+    return {"counts": c, "scores": redundancy_scores(c, n),
+            "retained": evict_by_score(c, budget, n_sink, n_recent)}
+
+
+# ----------------------------------------------------------------------------
+# Sec. 2, Fig. 1b: prevalence of twins
+# ----------------------------------------------------------------------------
+def prevalence(best_all: np.ndarray, taus) -> np.ndarray:
+    """Number of tokens with at least one twin for each threshold: a token has a twin at
+    tau exactly when its best similarity outside the window exceeds tau (Eq. 2), and a
+    token without any candidate (best = -1, reading R2) has none for tau >= -1."""
+    b = np.asarray(best_all, dtype=np.float64)
+    return np.array([int(np.sum(b > float(t))) for t in taus], dtype=np.int64)

@@ -268,9 +268,117 @@ def pin_budget_checked(o):
     raise AssertionError("budget != |S0| was accepted")
 
 
+# ----------------------------------------------------------------------------
+# Eq. 2-3 scorer and the Fig. 1b prevalence
+# ----------------------------------------------------------------------------
+def pin_twin_counts_golden(o):
+    fx = _load("twin_counts.json")
+    K = _one_hot_keys(fx["group"], fx["d"])
+    for case in fx["cases"]:
+        c = o.twin_counts(K, "f32", fx["tau"], case["w"])["counts"]
+        np.testing.assert_array_equal(c, case["counts"])
+    st = fx["strict"]
+    K = np.asarray(st["keys"], dtype=np.float32)
+    np.testing.assert_array_equal(o.twin_counts(K, "f32", 0.5, st["w"])["counts"], st["counts_at_0.5"])
+    np.testing.assert_array_equal(o.twin_counts(K, "f32", 0.4999, st["w"])["counts"],
+                                  st["counts_at_0.4999"])
+
+
+def _brute_counts(K, tau, w):
+    """Pure-Python Eq. 2 on a tiny input: its own normalisation and dot products."""
+    import math
+    n = len(K)
+    norms = [math.sqrt(math.fsum(float(x) * float(x) for x in k)) for k in K]
+    out = []
+    for i in range(n):
+        c = 0
+        for j in range(n):
+            if abs(i - j) <= w or norms[i] == 0.0 or norms[j] == 0.0:
+                continue
+            s = math.fsum(float(a) * float(b) for a, b in zip(K[i], K[j])) / (norms[i] * norms[j])
+            assert abs(s - tau) > 1e-9, "brute-force case too close to the threshold"
+            c += s > tau
+        out.append(c)
+    return out
+
+
+def pin_twin_counts_brute_force(o):
+    rng = np.random.default_rng(11)
+    for trial in range(6):
+        n, d, w = 14, 4, int(rng.integers(0, 4))
+        K = rng.standard_normal((n, d)).astype(np.float32)
+        for _ in range(3):                      # a few near-copies, so counts are not all 0
+            a, b = rng.choice(n, 2, replace=False)
+            K[b] = K[a] + np.float32(0.05) * rng.standard_normal(d).astype(np.float32)
+        tau = float(rng.choice([0.0, 0.3, 0.8, 0.95]))
+        np.testing.assert_array_equal(o.twin_counts(K, "f32", tau, w)["counts"],
+                                      _brute_counts(K.tolist(), tau, w))
+
+
+def pin_twin_counts_vs_best(o):
+    """A token has a twin (r_i >= 1) exactly when its best similarity outside the window
+    exceeds tau: the count path and the max path must agree; pairs are counted from both
+    sides, so the counts sum to an even number."""
+    rng = np.random.default_rng(12)
+    K = rng.standard_normal((300, 8)).astype(np.float32)
+    src = rng.integers(0, 280, 40)
+    K[src + rng.integers(5, 20, 40)] = K[src] + np.float32(0.05) * rng.standard_normal((40, 8)).astype(np.float32)
+    for tau in (0.5, 0.9, 0.99):
+        for w in (0, 3, 10):
+            c = o.twin_counts(K, "f32", tau, w)["counts"]
+            b = o.nn_scores(K, "f32", None, w)["best_all"]
+            np.testing.assert_array_equal(c >= 1, b > tau)
+            assert int(c.sum()) % 2 == 0
+
+
+def pin_scores_eq3(o):
+    c = np.array([0, 1, 5, 2])
+    np.testing.assert_allclose(o.redundancy_scores(c, 8), [0.0, -0.125, -0.625, -0.25], rtol=0, atol=0)
+
+
+def pin_evict_golden(o):
+    fx = _load("evict_ranked.json")
+    for case in fx["cases"]:
+        got = o.evict_by_score(np.asarray(fx["counts"]), case["budget"], fx["n_sink"], fx["n_recent"])
+        np.testing.assert_array_equal(got, case["retained"])
+
+
+def pin_evict_invariants(o):
+    """Budget exactly met, protected regions kept, every kept token scores at least as high
+    as every evicted one, and at the cut the later positions are the kept ones."""
+    rng = np.random.default_rng(13)
+    for trial in range(200):
+        n = int(rng.integers(1, 40))
+        counts = rng.integers(0, 4, n)          # many exact ties
+        n_sink, n_recent = int(rng.integers(0, 4)), int(rng.integers(0, 4))
+        budget = int(rng.integers(0, n + 3))
+        keep = o.evict_by_score(counts, budget, n_sink, n_recent).astype(bool)
+        assert keep.sum() == min(budget, n)
+        idx = np.arange(n)
+        prot = (idx < n_sink) | (idx >= n - n_recent)
+        if budget >= prot.sum():
+            assert keep[prot].all()
+        free = ~prot
+        kept, ev = keep & free, ~keep & free
+        if kept.any() and ev.any():
+            assert counts[kept].max() <= counts[ev].min()
+            cut = counts[kept].max()
+            if (ev & (counts == cut)).any():
+                assert idx[kept & (counts == cut)].min() > idx[ev & (counts == cut)].max()
+        if budget < prot.sum():
+            assert not keep[free].any()
+
+
+def pin_prevalence_golden(o):
+    fx = _load("prevalence.json")
+    np.testing.assert_array_equal(o.prevalence(np.asarray(fx["best"]), fx["taus"]), fx["counts"])
+
+
 ALL_PINS = [
     pin_closed_forms, pin_window_and_sentinel, pin_scale_invariance, pin_bf16_decode,
     pin_nonfinite_rejected, pin_repair_ranked, pin_oscillation, pin_repair_invariants,
     pin_exact_noops, pin_redundancy_consistent_noop, pin_second_pass_condition,
     pin_budget_checked,
+    pin_twin_counts_golden, pin_twin_counts_brute_force, pin_twin_counts_vs_best,
+    pin_scores_eq3, pin_evict_golden, pin_evict_invariants, pin_prevalence_golden,
 ]

@@ -46,6 +46,21 @@ MUTANTS = {
                          "k = (np.asarray(keys, dtype=np.uint16).astype(np.uint32) << 15).view(np.float32)"),
     "nonfinite_allowed": ("if not np.all(np.isfinite(k)):", "if False:"),
     "budget_unchecked": ("if int(s0.sum()) != int(budget):", "if False:"),
+    # Eq. 2-3 scorer and the prevalence statistic
+    "count_ge": ('out["counts"][a:a + step] = np.sum(valid & (S > tau), axis=1)',
+                 'out["counts"][a:a + step] = np.sum(valid & (S >= tau), axis=1)'),
+    "count_window_ignored": ('out["counts"][a:a + step] = np.sum(valid & (S > tau), axis=1)',
+                             'out["counts"][a:a + step] = np.sum(S > tau, axis=1) - 1'),
+    "count_tau_scaled": ('out["counts"][a:a + step] = np.sum(valid & (S > tau), axis=1)',
+                         'out["counts"][a:a + step] = np.sum(valid & (S > tau * 0.99), axis=1)'),
+    "score_sign": ("return -np.asarray(counts, dtype=np.float64) / float(n)",
+                   "return np.asarray(counts, dtype=np.float64) / float(n)"),
+    "evict_ascending": ("order = np.lexsort((-pos, -score))", "order = np.lexsort((-pos, score))"),
+    "evict_tie_earlier": ("order = np.lexsort((-pos, -score))", "order = np.lexsort((pos, -score))"),
+    "evict_unprotected": ("score = np.where(protected_mask(n, n_sink, n_recent), np.inf, redundancy_scores(counts, n))",
+                          "score = redundancy_scores(counts, n)"),
+    "evict_budget_off_by_one": ("keep[order[:min(budget, n)]] = 1", "keep[order[:min(budget + 1, n)]] = 1"),
+    "prevalence_ge": ("np.sum(b > float(t))", "np.sum(b >= float(t))"),
 }
 
 
