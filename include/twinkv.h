@@ -9,7 +9,10 @@
  *   - repair (Sec. 3.4): orphans (i not in S0, b_i < tau) and redundant donors (j in S0,
  *     outside the protected sink / recent regions, b_j >= tau) are ranked by severity
  *     (orphans by ascending b, donors by descending b) and the m = min(|O|, |D|) most severe
- *     pairs are swapped, so |S1| = |S0| = K exactly.
+ *     pairs are swapped, so |S1| = |S0| = K exactly;
+ *   - the standalone scorer (Sec. 3.2, Eq. 2-3): twin counts r_i, scores s_i = -r_i / n, and
+ *     the retained set of the K highest scores with the sink / recent regions kept first;
+ *   - the prevalence statistic of Sec. 2 (Fig. 1b): tokens with at least one twin.
  *
  * Problems.  A batch holds n_heads (layer, KV head) pairs times n_seqs sequences.  Sequence s
  * owns global token positions [cu_seqlens[s], cu_seqlens[s+1]) and T = cu_seqlens[n_seqs].
@@ -57,6 +60,11 @@ extern "C" {
 #define TWINKV_OP_NN_SCORES          0
 #define TWINKV_OP_REPAIR             1
 #define TWINKV_OP_REPAIR_FROM_SCORES 2
+#define TWINKV_OP_TWIN_COUNTS        3
+#define TWINKV_OP_SCORE_EVICT        4
+
+/* Most thresholds twinkv_prevalence takes in one call. */
+#define TWINKV_MAX_TAUS 32
 
 /* Per-problem status codes (stats[q][3] / status[q]). */
 #define TWINKV_PROBLEM_OK              0
@@ -66,7 +74,7 @@ extern "C" {
 /*
  * Bytes of workspace `op` needs for this batch; negative (-TWINKV_E_*) on invalid arguments.
  * cu_seqlens (host, n_seqs + 1 entries, non-decreasing, cu_seqlens[0] = 0).
- * dtype and d are ignored for TWINKV_OP_REPAIR_FROM_SCORES.
+ * dtype and d are ignored for TWINKV_OP_REPAIR_FROM_SCORES.  twinkv_prevalence needs none.
  */
 int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs,
                                const int64_t* cu_seqlens);
@@ -134,6 +142,63 @@ int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_
                               const int64_t* budget, float tau, int n_sink, int n_recent,
                               int32_t* stats,
                               void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * Twin counts of Sec. 3.2 Eq. 2 for every token:
+ *   counts[h][t] = #{ j in t's sequence : |i - j| > w, sim(i, j) > tau },  i = t's position.
+ *
+ *   keys, dtype, d, n_heads, n_seqs, cu_seqlens, strides, w   as in twinkv_nn_scores.
+ *   tau      twin threshold (finite).
+ *   counts   [n_heads][T] int32 (required).
+ *   status   [n_heads * n_seqs] int32 TWINKV_PROBLEM_* (only OK / NONFINITE).  Nullable.
+ *   workspace  twinkv_workspace_bytes(TWINKV_OP_TWIN_COUNTS, ...) bytes.
+ *
+ * The decision sim > tau is taken on fp32 similarities (error below 1e-4, typically 1e-6):
+ * pairs whose exact similarity is that close to tau may fall on either side.
+ */
+int twinkv_twin_counts(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                       const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                       float tau, int w, int32_t* counts, int32_t* status,
+                       void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * The standalone TwinKV scorer of Sec. 3.2: Eq. 2 twin counts, Eq. 3 scores
+ * s_i = -r_i / n (n = the sequence length), and the retained set of the `budget` highest
+ * scores.  The sink region [0, n_sink) and recent region [len - n_recent, len) take the
+ * maximum score, so they are kept first; among equal scores the later position is kept
+ * first (recency).  With budget >= len every token is kept; with budget 0 none.
+ *
+ *   budget        (host) [n_seqs] int64 >= 0: tokens to keep per problem of sequence s (the
+ *                 paper's ceil((1 - rho) n) for compression ratio rho is the caller's).
+ *   retained_out  [n_heads][T] uint8, receives the kept set as 0/1 (required).
+ *   counts        [n_heads][T] int32, the Eq. 2 counts.  Nullable (then kept in workspace).
+ *   scores        [n_heads][T] fp32, the Eq. 3 scores.  Nullable.
+ *   stats         [n_heads * n_seqs][4] int32 = {tokens kept, count at the cut (-1 when the
+ *                 cut falls inside the protected regions or nothing is cut), status, 0}.
+ *   workspace     twinkv_workspace_bytes(TWINKV_OP_SCORE_EVICT, ...) bytes.
+ * Other arguments as in twinkv_twin_counts.
+ */
+int twinkv_score_evict(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                       const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                       const int64_t* budget, float tau, int w, int n_sink, int n_recent,
+                       uint8_t* retained_out, int32_t* counts, float* scores, int32_t* stats,
+                       void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * Twin prevalence (Sec. 2, Fig. 1b): for every problem q and threshold taus[k],
+ *   out[q][k] = #{ tokens i of q : best_all[i] > taus[k] },
+ * the number of tokens with at least one twin at that threshold (Eq. 2), from best_all as
+ * produced by twinkv_nn_scores or twinkv_repair.
+ *
+ *   best_all  [n_heads][T] fp32.
+ *   taus      (host) [n_taus] fp32, 1 <= n_taus <= TWINKV_MAX_TAUS.
+ *   out       [n_heads * n_seqs][n_taus] int32.
+ *   workspace  twinkv_workspace_bytes(TWINKV_OP_REPAIR_FROM_SCORES, ...) bytes (the sequence
+ *              table).
+ */
+int twinkv_prevalence(const float* best_all, int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                      const float* taus, int n_taus, int32_t* out,
+                      void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
  * Profiling hook.  For calls made afterwards from the calling thread, record the given

@@ -21,7 +21,8 @@ LIB_PATH = os.path.join(_HERE, "libtwinkv.so")
 
 TWINKV_OK = 0
 TWINKV_BF16, TWINKV_F32 = 0, 1
-OP_NN_SCORES, OP_REPAIR, OP_REPAIR_FROM_SCORES = 0, 1, 2
+OP_NN_SCORES, OP_REPAIR, OP_REPAIR_FROM_SCORES, OP_TWIN_COUNTS, OP_SCORE_EVICT = 0, 1, 2, 3, 4
+MAX_TAUS = 32
 PROBLEM_OK, PROBLEM_BUDGET_MISMATCH, PROBLEM_NONFINITE = 0, 1, 2
 
 _lib = None
@@ -40,6 +41,12 @@ SIGNATURES = {
                            _VP, _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_repair_from_scores": (_I, [_VP, _VP, _VP, _I, _I, _PI64, _PI64, _F, _I, _I, _VP,
                                        _VP, _I64, _VP]),
+    "twinkv_twin_counts": (_I, [_VP, _I, _I, _I, _I, _PI64, _I64, _I64, _F, _I, _VP, _VP, _VP,
+                                _I64, _VP]),
+    "twinkv_score_evict": (_I, [_VP, _I, _I, _I, _I, _PI64, _I64, _I64, _PI64, _F, _I, _I, _I,
+                                _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
+    "twinkv_prevalence": (_I, [_VP, _I, _I, _PI64, ctypes.POINTER(ctypes.c_float), _I, _VP, _VP,
+                               _I64, _VP]),
     "twinkv_status_string": (ctypes.c_char_p, [_I]),
     "twinkv_version": (_I, []),
     "twinkv_profile_sim_events": (None, [_VP, _VP]),
@@ -267,3 +274,82 @@ def repair_from_scores(b, retained, budget, tau: float, n_sink: int = 4, n_recen
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_repair_from_scores", rc)
     return {"s1": s1, "stats": stats}
+
+
+def twin_counts(keys, tau: float, w: int = 32, cu_seqlens=None, *, workspace=None) -> dict:
+    """Eq. 2 twin counts r_i (int32, (n_heads, T)) and a per-problem status."""
+    torch = _torch()
+    keys, dt = _prep_keys(keys)
+    H, T, d = keys.shape
+    dev = keys.device
+    cu = _cu(cu_seqlens, T)
+    if cu[-1] != T:
+        raise ValueError("cu_seqlens[-1] must equal T")
+    counts = torch.empty((H, T), dtype=torch.int32, device=dev)
+    status = torch.empty((H * (len(cu) - 1),), dtype=torch.int32, device=dev)
+    nbytes = workspace_bytes(OP_TWIN_COUNTS, dt, d, H, cu)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
+        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    rc = lib().twinkv_twin_counts(
+        keys.data_ptr(), dt, d, H, len(cu) - 1, _i64_array(cu), keys.stride(0), keys.stride(1),
+        float(tau), int(w), counts.data_ptr(), status.data_ptr(), ws.data_ptr(), ws.numel(),
+        _stream(dev))
+    if rc != TWINKV_OK:
+        raise TwinKVError("twinkv_twin_counts", rc)
+    return {"counts": counts, "status": status}
+
+
+def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent: int = 64,
+                cu_seqlens=None, *, want_scores: bool = True, workspace=None) -> dict:
+    """The standalone scorer of Sec. 3.2: counts (Eq. 2), scores (Eq. 3), the kept set of the
+    `budget` highest scores (uint8) and per-problem stats {kept, count at cut, status, 0}."""
+    torch = _torch()
+    keys, dt = _prep_keys(keys)
+    H, T, d = keys.shape
+    dev = keys.device
+    cu = _cu(cu_seqlens, T)
+    n_seqs = len(cu) - 1
+    bud = np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,)).copy()
+    out = {
+        "retained": torch.empty((H, T), dtype=torch.uint8, device=dev),
+        "counts": torch.empty((H, T), dtype=torch.int32, device=dev),
+        "scores": torch.empty((H, T), dtype=torch.float32, device=dev) if want_scores else None,
+        "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
+    }
+    nbytes = workspace_bytes(OP_SCORE_EVICT, dt, d, H, cu)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
+        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    rc = lib().twinkv_score_evict(
+        keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
+        _i64_array(bud), float(tau), int(w), int(n_sink), int(n_recent),
+        out["retained"].data_ptr(), out["counts"].data_ptr(), _ptr(out["scores"]),
+        out["stats"].data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev))
+    if rc != TWINKV_OK:
+        raise TwinKVError("twinkv_score_evict", rc)
+    return {k: v for k, v in out.items() if v is not None}
+
+
+def prevalence(best_all, taus, cu_seqlens=None) -> "torch.Tensor":
+    """Tokens with at least one twin (best_all > tau) per problem and threshold:
+    int32 (n_heads * n_seqs, len(taus))."""
+    torch = _torch()
+    if best_all.dim() == 1:
+        best_all = best_all.unsqueeze(0)
+    if best_all.dtype != torch.float32 or not best_all.is_cuda:
+        raise ValueError("best_all must be a float32 GPU tensor")
+    best_all = best_all.contiguous()
+    H, T = best_all.shape
+    dev = best_all.device
+    cu = _cu(cu_seqlens, T)
+    n_seqs = len(cu) - 1
+    tv = np.ascontiguousarray(np.asarray(taus, dtype=np.float32))
+    out = torch.empty((H * n_seqs, len(tv)), dtype=torch.int32, device=dev)
+    nbytes = workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu)
+    ws = torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    rc = lib().twinkv_prevalence(
+        best_all.data_ptr(), H, n_seqs, _i64_array(cu),
+        tv.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(tv), out.data_ptr(),
+        ws.data_ptr(), ws.numel(), _stream(dev))
+    if rc != TWINKV_OK:
+        raise TwinKVError("twinkv_prevalence", rc)
+    return out

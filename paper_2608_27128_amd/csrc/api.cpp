@@ -70,8 +70,8 @@ Layout layout_for(int op, int dtype, int d, const Batch& bt) {
     }
     L.pkeys = off;
     off = align_up(off + 2 * np * dcol);
-    if (op == TWINKV_OP_REPAIR) {
-      L.bbuf = off;
+    if (op == TWINKV_OP_REPAIR || op == TWINKV_OP_SCORE_EVICT) {
+      L.bbuf = off;  // b for the repair pass, the twin counts for the scorer
       off = align_up(off + 4 * nt);
     }
   }
@@ -136,7 +136,8 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
                const int64_t* budget, int64_t head_stride, int64_t token_stride,
                const uint8_t* retained, int w, float* best_all, int32_t* arg_all,
                float* best_ret, int32_t* arg_ret, int32_t* status, char* ws, const Layout& L,
-               bool want_all, void* stream, SeqInfo** seqtab_dev) {
+               bool want_all, void* stream, SeqInfo** seqtab_dev, float tau = 0.0f,
+               int32_t* counts = nullptr) {
   int total_tiles = 0;
   const int rpb = sim_rows_per_block(dtype, d);
   std::vector<SeqInfo> tab = seq_table(cu, bt.n_seqs, budget, rpb, total_tiles);
@@ -191,6 +192,8 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
   // |i - j| <= T - 1 inside any sequence, so any w >= T behaves like w = T.
   a.w = (int)std::min<int64_t>(w, std::max<int64_t>(bt.T, 1));
   a.want_all = want_all ? 1 : 0;
+  a.tau = tau;
+  a.counts = counts;
   a.total_tiles = total_tiles;
   a.best_all = best_all;
   a.arg_all = arg_all;
@@ -212,7 +215,8 @@ extern "C" {
 
 int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs,
                                const int64_t* cu_seqlens) {
-  if (op != TWINKV_OP_NN_SCORES && op != TWINKV_OP_REPAIR && op != TWINKV_OP_REPAIR_FROM_SCORES)
+  if (op != TWINKV_OP_NN_SCORES && op != TWINKV_OP_REPAIR && op != TWINKV_OP_REPAIR_FROM_SCORES &&
+      op != TWINKV_OP_TWIN_COUNTS && op != TWINKV_OP_SCORE_EVICT)
     return -TWINKV_E_ARG;
   if (op != TWINKV_OP_REPAIR_FROM_SCORES) {
     if (dtype != TWINKV_BF16 && dtype != TWINKV_F32) return -TWINKV_E_UNSUPPORTED;
@@ -331,6 +335,95 @@ int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_
   ra.n_recent = n_recent;
   ra.stats = stats;
   return hip_status(launch_repair(ra, stream));
+}
+
+int twinkv_twin_counts(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                       const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                       float tau, int w, int32_t* counts, int32_t* status, void* workspace,
+                       int64_t workspace_bytes, void* stream) {
+  int rc = check_keys(keys, dtype, d, head_stride, token_stride, w);
+  if (rc != TWINKV_OK) return rc;
+  Batch bt;
+  rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  if (counts == nullptr) return TWINKV_E_NULL;
+  if (!std::isfinite(tau)) return TWINKV_E_ARG;
+  const Layout L = layout_for(TWINKV_OP_TWIN_COUNTS, dtype, d, bt);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+  SeqInfo* dtab = nullptr;
+  // every column is an "evicted" column (no retained set): one all-keys sweep that counts
+  return run_scores(keys, dtype, d, bt, cu_seqlens, nullptr, head_stride, token_stride, nullptr,
+                    w, nullptr, nullptr, nullptr, nullptr, status, ws, L, /*want_all=*/true,
+                    stream, &dtab, tau, counts);
+}
+
+int twinkv_score_evict(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                       const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                       const int64_t* budget, float tau, int w, int n_sink, int n_recent,
+                       uint8_t* retained_out, int32_t* counts, float* scores, int32_t* stats,
+                       void* workspace, int64_t workspace_bytes, void* stream) {
+  int rc = check_keys(keys, dtype, d, head_stride, token_stride, w);
+  if (rc != TWINKV_OK) return rc;
+  Batch bt;
+  rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  if (retained_out == nullptr || budget == nullptr || stats == nullptr) return TWINKV_E_NULL;
+  if (!std::isfinite(tau) || n_sink < 0 || n_recent < 0) return TWINKV_E_ARG;
+  for (int s = 0; s < n_seqs; ++s) {
+    if (budget[s] < 0 || budget[s] > INT32_MAX) return TWINKV_E_ARG;
+  }
+  const Layout L = layout_for(TWINKV_OP_SCORE_EVICT, dtype, d, bt);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+  int32_t* c = counts ? counts : reinterpret_cast<int32_t*>(ws + L.bbuf);
+  SeqInfo* dtab = nullptr;
+  rc = run_scores(keys, dtype, d, bt, cu_seqlens, budget, head_stride, token_stride, nullptr, w,
+                  nullptr, nullptr, nullptr, nullptr, nullptr, ws, L, /*want_all=*/true, stream,
+                  &dtab, tau, c);
+  if (rc != TWINKV_OK) return rc;
+  EvictArgs ea;
+  ea.counts = c;
+  ea.retained = retained_out;
+  ea.scores = scores;
+  ea.stats = stats;
+  ea.seqtab = dtab;
+  ea.pmeta = reinterpret_cast<const ProblemMeta*>(ws + L.pmeta);
+  ea.n_heads = n_heads;
+  ea.n_seqs = n_seqs;
+  ea.T = bt.T;
+  ea.n_sink = n_sink;
+  ea.n_recent = n_recent;
+  return hip_status(launch_evict(ea, stream));
+}
+
+int twinkv_prevalence(const float* best_all, int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                      const float* taus, int n_taus, int32_t* out, void* workspace,
+                      int64_t workspace_bytes, void* stream) {
+  if (best_all == nullptr || taus == nullptr || out == nullptr) return TWINKV_E_NULL;
+  if (n_taus < 1 || n_taus > kMaxTaus) return TWINKV_E_ARG;
+  Batch bt;
+  int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  const Layout L = layout_for(TWINKV_OP_REPAIR_FROM_SCORES, 0, 64, bt);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+  int tiles = 0;
+  std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, nullptr, 0, tiles);
+  SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
+  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
+                     (hipStream_t)stream) != hipSuccess)
+    return TWINKV_E_HIP;
+  PrevalenceArgs pa;
+  pa.best = best_all;
+  pa.out = out;
+  pa.seqtab = dtab;
+  pa.n_heads = n_heads;
+  pa.n_seqs = n_seqs;
+  pa.T = bt.T;
+  pa.n_taus = n_taus;
+  for (int k = 0; k < kMaxTaus; ++k) pa.taus[k] = k < n_taus ? taus[k] : 0.0f;
+  return hip_status(launch_prevalence(pa, stream));
 }
 
 const char* twinkv_status_string(int status) {

@@ -1,0 +1,175 @@
+// K4: the standalone scorer's eviction (Sec. 3.2) and the twin prevalence statistic
+// (Sec. 2, Fig. 1b), one problem per workgroup.
+//
+// Eviction: the score is s_i = -r_i / n (Eq. 3), the sink and recent regions score highest,
+// and the `budget` highest scores are retained; equal scores go to the later position first.
+// Ranking by the key  0 for protected positions, r_i + 1 otherwise  (ascending) gives the
+// same order.  The budget-th smallest key is found by an MSB-first 8-bit radix select with
+// LDS histograms; a block-wide scan in position order then keeps the last members equal to
+// that key.  Every pass streams the counts (4 bytes per token).
+//
+// Prevalence: for each threshold tau_k, the number of tokens whose best similarity outside
+// the window exceeds tau_k, i.e. that have at least one twin (Eq. 2).
+#include <hip/hip_runtime.h>
+
+#include "../twinkv_internal.h"
+
+namespace twinkv {
+namespace {
+
+constexpr int kEvThreads = 256;
+
+// Exclusive prefix sum over the block; `total` receives the block sum.
+__device__ inline int ev_exclusive_scan(int v, int* s_wave, int& total) {
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) s_wave[wv] = x;
+  __syncthreads();
+  int base = 0;
+  total = 0;
+#pragma unroll
+  for (int k = 0; k < kEvThreads / 64; ++k) {
+    const int t = s_wave[k];
+    base += (k < wv) ? t : 0;
+    total += t;
+  }
+  __syncthreads();
+  return base + x - v;
+}
+
+__global__ __launch_bounds__(kEvThreads) void evict_kernel(EvictArgs a) {
+  __shared__ int s_wave[kEvThreads / 64];
+  __shared__ int s_hist[256];
+  __shared__ int s_digit, s_before;
+
+  const int q = blockIdx.x;
+  const int h = q / a.n_seqs;
+  const int s = q - h * a.n_seqs;
+  const SeqInfo si = a.seqtab[s];
+  const int len = si.len;
+  const int64_t base = (int64_t)h * a.T + si.start;
+  const int32_t* cnt = a.counts + base;
+  uint8_t* out = a.retained + base;
+  const int rec0 = len - a.n_recent;
+  const int tid = threadIdx.x;
+  const int budget = si.budget < len ? si.budget : len;
+  auto key_of = [&](int t) -> uint32_t {
+    return (t < a.n_sink || t >= rec0) ? 0u : (uint32_t)cnt[t] + 1u;
+  };
+
+  // ---- radix select of the budget-th smallest key ----
+  uint32_t key_cut = 0u;
+  int take_eq = 0;
+  const bool cut = budget > 0 && budget < len;
+  if (cut) {
+    uint32_t prefix = 0, mask = 0;
+    int kk = budget;  // 1-based rank still to find among keys matching `prefix`
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      s_hist[tid] = 0;
+      __syncthreads();
+      for (int t = tid; t < len; t += kEvThreads) {
+        const uint32_t key = key_of(t);
+        if ((key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+      }
+      __syncthreads();
+      const int hcount = s_hist[tid];
+      int dummy;
+      const int before = ev_exclusive_scan(hcount, s_wave, dummy);
+      if (before < kk && kk <= before + hcount) {
+        s_digit = tid;
+        s_before = before;
+      }
+      __syncthreads();
+      kk -= s_before;
+      prefix |= (uint32_t)s_digit << shift;
+      mask |= 0xFFu << shift;
+      __syncthreads();
+    }
+    key_cut = prefix;
+    take_eq = kk;  // members equal to key_cut still to keep: the last ones by position
+  }
+
+  // ---- final pass: contiguous ranges per thread so equal keys are ranked by position ----
+  const int span = (len + kEvThreads - 1) / kEvThreads;
+  const int t0 = min(len, tid * span);
+  const int t1 = min(len, t0 + span);
+  int eq_here = 0;
+  if (cut)
+    for (int t = t0; t < t1; ++t) eq_here += key_of(t) == key_cut;
+  int total_eq;
+  int eq_rank = ev_exclusive_scan(eq_here, s_wave, total_eq);
+  const float inv_n = len > 0 ? 1.0f / (float)len : 0.0f;
+  for (int t = t0; t < t1; ++t) {
+    uint8_t keep;
+    if (!cut) {
+      keep = budget > 0 ? 1 : 0;
+    } else {
+      const uint32_t key = key_of(t);
+      if (key < key_cut) keep = 1;
+      else if (key == key_cut) keep = (eq_rank++ >= total_eq - take_eq) ? 1 : 0;
+      else keep = 0;
+    }
+    out[t] = keep;
+    if (a.scores) a.scores[base + t] = -(float)cnt[t] * inv_n;
+  }
+  if (tid == 0) {
+    int32_t* st = a.stats + 4 * (int64_t)q;
+    st[0] = budget;
+    st[1] = cut ? (key_cut == 0u ? -1 : (int32_t)(key_cut - 1u)) : -1;
+    st[2] = (a.pmeta && (a.pmeta[q].flags & kFlagNonfinite)) ? 2 : 0;
+    st[3] = 0;
+  }
+}
+
+__global__ __launch_bounds__(kEvThreads) void prevalence_kernel(PrevalenceArgs a) {
+  __shared__ int s_cnt[kMaxTaus];
+  const int q = blockIdx.x;
+  const int h = q / a.n_seqs;
+  const int s = q - h * a.n_seqs;
+  const SeqInfo si = a.seqtab[s];
+  const float* b = a.best + (int64_t)h * a.T + si.start;
+  if (threadIdx.x < kMaxTaus) s_cnt[threadIdx.x] = 0;
+  __syncthreads();
+  int c[kMaxTaus];
+#pragma unroll
+  for (int k = 0; k < kMaxTaus; ++k) c[k] = 0;
+  for (int t = threadIdx.x; t < si.len; t += kEvThreads) {
+    const float x = b[t];
+#pragma unroll
+    for (int k = 0; k < kMaxTaus; ++k) c[k] += (k < a.n_taus && x > a.taus[k]) ? 1 : 0;
+  }
+#pragma unroll
+  for (int k = 0; k < kMaxTaus; ++k) {
+    int v = c[k];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if ((threadIdx.x & 63) == 0 && k < a.n_taus) atomicAdd(&s_cnt[k], v);
+  }
+  __syncthreads();
+  if (threadIdx.x < a.n_taus) a.out[(int64_t)q * a.n_taus + threadIdx.x] = s_cnt[threadIdx.x];
+}
+
+}  // namespace
+
+int launch_evict(const EvictArgs& a, void* stream) {
+  const int64_t P = (int64_t)a.n_heads * a.n_seqs;
+  if (P == 0) return hipSuccess;
+  hipLaunchKernelGGL(evict_kernel, dim3((unsigned)P), dim3(kEvThreads), 0, (hipStream_t)stream, a);
+  return hipGetLastError();
+}
+
+int launch_prevalence(const PrevalenceArgs& a, void* stream) {
+  const int64_t P = (int64_t)a.n_heads * a.n_seqs;
+  if (P == 0) return hipSuccess;
+  hipLaunchKernelGGL(prevalence_kernel, dim3((unsigned)P), dim3(kEvThreads), 0,
+                     (hipStream_t)stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace twinkv

@@ -4,7 +4,8 @@
 // N x N matrix (Sec. 3.2 Eq. 1 and the twin window; Sec. 3.4 Eq. 4):
 //   best over all j with |i-j| > w of sim(i, j)        -> best_all / arg_all
 //   best over j in S0 with |i-j| > w of sim(i, j)      -> best_ret / arg_ret  (= b_i(S0))
-// with sim(i, j) = (k_i . k_j) * r_i * r_j, r = 1 / ||k||.
+// with sim(i, j) = (k_i . k_j) * r_i * r_j, r = 1 / ||k||.  In count mode (Sec. 3.2 Eq. 2)
+// the same sweep instead counts, per token, the j with |i-j| > w and sim(i, j) > tau.
 //
 // Mapping onto gfx950:
 //  * One workgroup owns RB = NWAVES * NSUB * 32 consecutive rows of one problem; each wave
@@ -142,6 +143,19 @@ __device__ inline uint32_t chunk_best(const f32x16& acc, const float (&rv)[16]) 
   return b;
 }
 
+// Number of a lane's 16 similarities above the row's threshold (count mode, Eq. 2):
+// y = dot * r_j + c_i with c_i = -tau * g_i / r_i is positive exactly when sim(i, j) > tau
+// (a y of exactly +0, sim equal to tau up to fp32 rounding, counts as above).  Each sign
+// bit is shifted into a mask with one v_alignbit (a serial chain the compiler cannot
+// reassociate into a wide tree), and one v_bcnt counts them.
+__device__ inline uint32_t chunk_count(const f32x16& acc, const float (&rv)[16], float c_row) {
+  uint32_t neg = 0u;
+#pragma unroll
+  for (int v = 0; v < 16; ++v)
+    neg = __builtin_amdgcn_alignbit(neg, __float_as_uint(fmaf(acc[v], rv[v], c_row)), 31);
+  return 16u - (uint32_t)__builtin_popcount(neg);
+}
+
 // Branch-free running update: a strictly larger value (slot bits ignored) replaces the
 // running best, so an earlier chunk keeps exact ties.
 __device__ inline void run_update(uint32_t best, int gc, uint32_t& run, int& cid) {
@@ -150,7 +164,7 @@ __device__ inline void run_update(uint32_t best, int gc, uint32_t& run, int& cid
   cid = upd ? gc : cid;
 }
 
-template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC>
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC, bool COUNT>
 __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kernel(SimArgs a) {
   using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC>;
   static_assert(kGroupAlign % C::TN == 0, "the evicted group must start on a tile boundary");
@@ -254,11 +268,16 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
 
   // ---- row keys: MFMA B operands, resident for the whole sweep ------------------------
   bf16x8 bfrag[NSUB][C::KSTEPS];
+  // Count mode: sim(i, j) > tau  <=>  dot * r_j - tau * g_i / r_i > 0  (per row; a zero key
+  // has similarity 0 to every key, so it counts every candidate exactly when tau < 0).
+  float thr[NSUB];
 #pragma unroll
   for (int s = 0; s < NSUB; ++s) {
     const int i = wrow0 + s * 32 + l32;
     const bool ok = i < len;
-    const float g = row_scale(ok ? rinv[i] : 0.0f);
+    const float ri = ok ? rinv[i] : 0.0f;
+    const float g = row_scale(ri);
+    thr[s] = ri > 0.0f ? -a.tau * g / ri : (a.tau < 0.0f ? INFINITY : -INFINITY);
 #pragma unroll
     for (int t = 0; t < C::KSTEPS; ++t) {
       uint4 raw = make_uint4(0, 0, 0, 0);
@@ -365,8 +384,12 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   uint32_t pmask = 0u;  // result mask of the pending chunk (zero: dropped)
 
   auto reduce_into = [&](const f32x16& acc, const float (&rv)[16], int gc, int s, uint32_t m) {
-    const uint32_t best = chunk_best(acc, rv) & m;
-    run_update(best, gc, run[s], cid[s]);
+    if constexpr (COUNT) {
+      run[s] += chunk_count(acc, rv, thr[s]) & m;
+    } else {
+      const uint32_t best = chunk_best(acc, rv) & m;
+      run_update(best, gc, run[s], cid[s]);
+    }
   };
 
   // One tile: each chain's epilogue runs beside the following chain's MFMAs, and the last
@@ -478,18 +501,28 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       for (int t = 0; t < C::KSTEPS; ++t)
         x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[t], bfrag[s][t], x, 0, 0, 0);
       const int i = wrow0 + s * 32 + l32;
-      uint32_t best = 0u;
+      if constexpr (COUNT) {
+        uint32_t c = 0u;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float y = fmaf(x[v], rv[v], 3.0f);
-        const uint32_t u = (__float_as_uint(y) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
-        const bool ok = (jv[v] >= 0) && (abs(i - jv[v]) > a.w);
-        best = max(best, ok ? u : 0u);
+        for (int v = 0; v < 16; ++v) {
+          const uint32_t ok = (uint32_t)(jv[v] >= 0) & (uint32_t)(abs(i - jv[v]) > a.w);
+          c += ok & ((~__float_as_uint(fmaf(x[v], rv[v], thr[s]))) >> 31);
+        }
+        rs[s] += c;
+      } else {
+        uint32_t best = 0u;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float y = fmaf(x[v], rv[v], 3.0f);
+          const uint32_t u = (__float_as_uint(y) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
+          const uint32_t ok = (uint32_t)(jv[v] >= 0) & (uint32_t)(abs(i - jv[v]) > a.w);
+          best = max(best, u & (0u - ok));
+        }
+        const bool upd = (best >> 4) > (rs[s] >> 4) ||
+                         ((best >> 4) == (rs[s] >> 4) && best >= kValidMin && gc < cs[s]);
+        rs[s] = upd ? best : rs[s];
+        cs[s] = upd ? gc : cs[s];
       }
-      const bool upd = (best >> 4) > (rs[s] >> 4) ||
-                       ((best >> 4) == (rs[s] >> 4) && best >= kValidMin && gc < cs[s]);
-      rs[s] = upd ? best : rs[s];
-      cs[s] = upd ? gc : cs[s];
     }
   };
   auto masked_range = [&](int l, int h, uint32_t (&rs)[NSUB], int (&cs)[NSUB]) {
@@ -519,6 +552,16 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   }
 
   // ---- resolve: lanes l and l+32 hold the same row over disjoint column halves ----------
+  if constexpr (COUNT) {
+    // the S0 group is empty in count mode: every column was swept as an evicted column
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) {
+      const int i = wrow0 + s * 32 + l32;
+      const uint32_t total = run[s] + __shfl_xor(run[s], 32);
+      if (half == 0 && i < len) a.counts[(int64_t)head * a.T + si.start + i] = (int32_t)total;
+    }
+    return;
+  }
 #pragma unroll
   for (int s = 0; s < NSUB; ++s) {
     const int i = wrow0 + s * 32 + l32;
@@ -568,8 +611,12 @@ hipError_t run(const SimArgs& a, hipStream_t st) {
   const int64_t groups = a.n_heads >= 8 ? 8LL * ((a.n_heads + 7) / 8) : (int64_t)a.n_heads;
   const int64_t blocks = groups * a.total_tiles;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC>), dim3((unsigned)blocks),
-                     dim3(C::NT), 0, st, a);
+  if (a.counts != nullptr)
+    hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC, true>),
+                       dim3((unsigned)blocks), dim3(C::NT), 0, st, a);
+  else
+    hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC, false>),
+                       dim3((unsigned)blocks), dim3(C::NT), 0, st, a);
   return hipGetLastError();
 }
 

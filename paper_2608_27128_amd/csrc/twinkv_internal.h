@@ -81,6 +81,8 @@ struct SimArgs {
   int64_t T, PT;
   int w;
   int want_all;              // also reduce over evicted columns (best_all / arg_all)
+  float tau;                 // count mode: the twin threshold of Eq. 2
+  int32_t* counts;           // non-null: count mode, [n_heads][T] twin counts (Eq. 2)
   int total_tiles;           // row-block tiles of all sequences (sum of nb)
   float* best_all;
   int32_t* arg_all;
@@ -90,7 +92,8 @@ struct SimArgs {
 
 // Rows covered by one workgroup of the similarity kernel for this (dtype, d).
 int sim_rows_per_block(int dtype, int d);
-// K2: fused MFMA similarity with the two masked row max / argmax reductions.
+// K2: fused MFMA similarity with the two masked row max / argmax reductions, or (counts set)
+// the per-token twin counts of Eq. 2 over all columns.
 int launch_sim_reduce(const SimArgs& a, int dtype, int d, void* stream);
 
 struct RepairArgs {
@@ -107,5 +110,32 @@ struct RepairArgs {
 };
 // K3: orphan / donor classification, radix selection of the m most severe, swap.
 int launch_repair(const RepairArgs& a, void* stream);
+
+struct EvictArgs {
+  const int32_t* counts;     // [n_heads][T] Eq. 2 twin counts
+  uint8_t* retained;         // [n_heads][T] out: kept set
+  float* scores;             // nullable [n_heads][T] out: Eq. 3 scores
+  int32_t* stats;            // [n_heads * n_seqs][4]
+  const SeqInfo* seqtab;     // budget per sequence in .budget
+  const ProblemMeta* pmeta;  // key status from the key preparation
+  int n_heads, n_seqs;
+  int64_t T;
+  int n_sink, n_recent;
+};
+// K4a: the standalone scorer's retained set (the budget highest Eq. 3 scores).
+int launch_evict(const EvictArgs& a, void* stream);
+
+constexpr int kMaxTaus = 32;
+struct PrevalenceArgs {
+  const float* best;         // [n_heads][T] best_all
+  int32_t* out;              // [n_heads * n_seqs][n_taus]
+  const SeqInfo* seqtab;
+  int n_heads, n_seqs;
+  int64_t T;
+  int n_taus;
+  float taus[kMaxTaus];
+};
+// K4b: tokens with at least one twin per threshold (best_all > tau).
+int launch_prevalence(const PrevalenceArgs& a, void* stream);
 
 }  // namespace twinkv

@@ -57,6 +57,9 @@ def test_workspace_bytes():
     assert L.twinkv_workspace_bytes(0, 0, 96, 8, 1, cu_arr([0, 10])) == -E_UNSUP
     assert L.twinkv_workspace_bytes(0, 5, 64, 8, 1, cu_arr([0, 10])) == -E_UNSUP
     assert L.twinkv_workspace_bytes(7, 0, 64, 8, 1, cu_arr([0, 10])) == -E_ARG
+    tc = L.twinkv_workspace_bytes(3, 0, 64, 8, 1, cu_arr([0, 1000]))
+    se = L.twinkv_workspace_bytes(4, 0, 64, 8, 1, cu_arr([0, 1000]))
+    assert tc == bf and se > tc           # the scorer adds the count buffer
     assert L.twinkv_workspace_bytes(0, 0, 64, 0, 1, cu_arr([0, 10])) == -E_ARG
     assert L.twinkv_workspace_bytes(0, 0, 64, 8, 2, cu_arr([0, 10, 5])) == -E_ARG
     assert L.twinkv_workspace_bytes(0, 0, 64, 8, 1, cu_arr([3, 10])) == -E_ARG
@@ -120,6 +123,49 @@ def test_repair_from_scores_validation():
     assert call(stats=None) == E_NULL
     assert call(tau=float("nan")) == E_ARG
     assert call(budget=(11,)) == E_ARG
+    assert call(wsb=0) == E_WS
+
+
+def test_twin_counts_validation():
+    L = binding.lib()
+
+    def call(keys=FAKE, d=64, tau=0.85, w=32, counts=FAKE, wsb=1 << 40):
+        return L.twinkv_twin_counts(keys, 0, d, 2, 1, cu_arr([0, 100]), 6400, 64, tau, w, counts,
+                                    None, FAKE, wsb, None)
+    assert call(keys=None) == E_NULL
+    assert call(counts=None) == E_NULL
+    assert call(tau=float("nan")) == E_ARG
+    assert call(w=-1) == E_ARG
+    assert call(d=96) == E_UNSUP
+    assert call(wsb=64) == E_WS
+
+
+def test_score_evict_validation():
+    L = binding.lib()
+
+    def call(budget=(30,), tau=0.85, ns=4, nr=8, rout=FAKE, stats=FAKE, wsb=1 << 40):
+        bud = cu_arr(list(budget)) if budget is not None else None
+        return L.twinkv_score_evict(FAKE, 0, 64, 2, 1, cu_arr([0, 100]), 6400, 64, bud, tau, 32, ns, nr,
+                                    rout, None, None, stats, FAKE, wsb, None)
+    assert call(budget=None) == E_NULL
+    assert call(rout=None) == E_NULL
+    assert call(stats=None) == E_NULL
+    assert call(budget=(-1,)) == E_ARG
+    assert call(tau=float("inf")) == E_ARG
+    assert call(ns=-1) == E_ARG
+    assert call(wsb=64) == E_WS
+
+
+def test_prevalence_validation():
+    L = binding.lib()
+    taus = (ctypes.c_float * 40)(*([0.5] * 40))
+
+    def call(best=FAKE, n=3, out=FAKE, wsb=1 << 30):
+        return L.twinkv_prevalence(best, 2, 1, cu_arr([0, 100]), taus, n, out, FAKE, wsb, None)
+    assert call(best=None) == E_NULL
+    assert call(out=None) == E_NULL
+    assert call(n=0) == E_ARG
+    assert call(n=33) == E_ARG                  # more thresholds than one call takes
     assert call(wsb=0) == E_WS
 
 
