@@ -132,6 +132,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="long_aniso_32k",
                     help="tiny | llama1b_8k | qwen4b_16k | long_aniso_32k | ragged_64x")
+    ap.add_argument("--path", default="repair", choices=["repair", "repair_s0", "scorer"],
+                    help="repair: the full repair pass (both reductions, the headline); "
+                         "repair_s0: the repair pass against retained columns only; "
+                         "scorer: the standalone scorer (Eq. 2 counts, Eq. 3 eviction)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -178,17 +182,31 @@ def main() -> int:
     ret = torch.from_numpy(batch.retained).to(dev)
     cu = batch.cu_seqlens
     lens = np.diff(cu).astype(np.float64)
-    pairs = float(sp.n_heads * np.sum(lens * lens))      # ordered key pairs per step
+    H, T = batch.retained.shape
+    dt_code = 0 if batch.dtype == "bf16" else 1
+    if args.path == "repair_s0":
+        # columns restricted to S0: N * K ordered pairs per problem (K = |S0|)
+        pairs = float(sp.n_heads * np.sum(lens * np.asarray(batch.budget, dtype=np.float64)))
+    else:
+        pairs = float(sp.n_heads * np.sum(lens * lens))  # ordered key pairs per step
     flops = 2.0 * batch.d * pairs                         # dense masked K K^T, per launch
 
-    def step(outputs=None, ws=None):
-        return binding.repair(keys, ret, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent, cu,
-                              outputs=outputs, workspace=ws)
+    if args.path in ("repair", "repair_s0"):
+        want_all = args.path == "repair"
 
-    out = step()
-    H, T = batch.retained.shape
-    ws = torch.empty((binding.workspace_bytes(binding.OP_REPAIR, 0 if batch.dtype == "bf16" else 1,
-                                              batch.d, H, cu),), dtype=torch.uint8, device=dev)
+        def step(outputs=None, ws=None):
+            return binding.repair(keys, ret, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent,
+                                  cu, want_all=want_all, outputs=outputs, workspace=ws)
+        ws = torch.empty((binding.workspace_bytes(binding.OP_REPAIR, dt_code, batch.d, H, cu),),
+                         dtype=torch.uint8, device=dev)
+    else:
+        def step(outputs=None, ws=None):
+            return binding.score_evict(keys, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent,
+                                       cu, outputs=outputs, workspace=ws)
+        ws = torch.empty((binding.workspace_bytes(binding.OP_SCORE_EVICT, dt_code, batch.d, H, cu),),
+                         dtype=torch.uint8, device=dev)
+
+    out = step(None, ws)
     for _ in range(args.warmup):
         step(out, ws)
     torch.cuda.synchronize()
@@ -214,11 +232,18 @@ def main() -> int:
     for e in k2_start + k2_stop:
         hev.destroy(e)
     stats = out["stats"].cpu().numpy()
-    assert (stats[:, 3] == 0).all(), "a problem reported a non-OK status"
-    s1_sum = out["s1"].sum(dim=1).cpu().numpy()
-    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (events {ev_ms:.3f}); "
-        f"similarity kernel {k2_ms:.3f} ms; swaps {int(stats[:, 2].sum())}; "
-        f"|S1| per head {int(s1_sum.min())}..{int(s1_sum.max())}")
+    if args.path == "scorer":
+        assert (stats[:, 2] == 0).all(), "a problem reported a non-OK status"
+        kept = out["retained"].sum(dim=1).cpu().numpy()
+        log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (events {ev_ms:.3f}); "
+            f"similarity kernel (count mode) {k2_ms:.3f} ms; kept per head "
+            f"{int(kept.min())}..{int(kept.max())}")
+    else:
+        assert (stats[:, 3] == 0).all(), "a problem reported a non-OK status"
+        s1_sum = out["s1"].sum(dim=1).cpu().numpy()
+        log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (events {ev_ms:.3f}); "
+            f"similarity kernel {k2_ms:.3f} ms; swaps {int(stats[:, 2].sum())}; "
+            f"|S1| per head {int(s1_sum.min())}..{int(s1_sum.max())}")
 
     achieved = flops / (k2_ms * 1e-3) / 1e12
     result = {
@@ -237,11 +262,12 @@ def main() -> int:
         "config": {"workload": sp.name, "problems": int(sp.n_heads * sp.n_seqs),
                    "layers_x_kv_heads": int(sp.n_heads), "seq_lens": sorted(set(int(x) for x in lens))[:4],
                    "d": int(batch.d), "tau": sp.tau, "w": sp.w, "n_sink": sp.n_sink,
-                   "n_recent": sp.n_recent, "budget": int(batch.budget[0]), "parallelism": "none"},
+                   "n_recent": sp.n_recent, "budget": int(batch.budget[0]), "path": args.path,
+                   "parallelism": "none"},
         "repair_ms_per_cache": ms_per_step,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": profiled_traffic(sp.name),
+                     "traffic": profiled_traffic(sp.name) if args.path == "repair" else None,
                      "kernel": "sim_reduce_kernel", "kernel_ms": k2_ms,
                      "flops_per_launch": flops},
     }

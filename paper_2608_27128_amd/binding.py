@@ -300,9 +300,11 @@ def twin_counts(keys, tau: float, w: int = 32, cu_seqlens=None, *, workspace=Non
 
 
 def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent: int = 64,
-                cu_seqlens=None, *, want_scores: bool = True, workspace=None) -> dict:
+                cu_seqlens=None, *, want_scores: bool = True, workspace=None,
+                outputs: Optional[dict] = None) -> dict:
     """The standalone scorer of Sec. 3.2: counts (Eq. 2), scores (Eq. 3), the kept set of the
-    `budget` highest scores (uint8) and per-problem stats {kept, count at cut, status, 0}."""
+    `budget` highest scores (uint8) and per-problem stats {kept, count at cut, status, 0}.
+    ``outputs`` may pass back the dict of an earlier call with the same shapes."""
     torch = _torch()
     keys, dt = _prep_keys(keys)
     H, T, d = keys.shape
@@ -310,12 +312,16 @@ def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent
     cu = _cu(cu_seqlens, T)
     n_seqs = len(cu) - 1
     bud = np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,)).copy()
-    out = {
-        "retained": torch.empty((H, T), dtype=torch.uint8, device=dev),
-        "counts": torch.empty((H, T), dtype=torch.int32, device=dev),
-        "scores": torch.empty((H, T), dtype=torch.float32, device=dev) if want_scores else None,
-        "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
-    }
+    if outputs is None:
+        out = {
+            "retained": torch.empty((H, T), dtype=torch.uint8, device=dev),
+            "counts": torch.empty((H, T), dtype=torch.int32, device=dev),
+            "scores": torch.empty((H, T), dtype=torch.float32, device=dev) if want_scores else None,
+            "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
+        }
+    else:
+        out = dict(outputs)
+        out.setdefault("scores", None)
     nbytes = workspace_bytes(OP_SCORE_EVICT, dt, d, H, cu)
     ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
         torch.empty((nbytes,), dtype=torch.uint8, device=dev)
