@@ -127,6 +127,12 @@ std::vector<SeqInfo> seq_table(const int64_t* cu, int n_seqs, const int64_t* bud
 
 int hip_status(int e) { return e == 0 ? TWINKV_OK : TWINKV_E_HIP; }
 
+int max_seq_len(const int64_t* cu, int n_seqs) {
+  int64_t m = 0;
+  for (int s = 0; s < n_seqs; ++s) m = std::max<int64_t>(m, cu[s + 1] - cu[s]);
+  return (int)m;
+}
+
 // Events recorded around the similarity kernel (twinkv_profile_sim_events), per thread.
 thread_local hipEvent_t g_sim_start = nullptr;
 thread_local hipEvent_t g_sim_stop = nullptr;
@@ -297,6 +303,7 @@ int twinkv_repair(const void* keys, int dtype, int d, int n_heads, int n_seqs,
   ra.n_sink = n_sink;
   ra.n_recent = n_recent;
   ra.stats = stats;
+  ra.max_len = max_seq_len(cu_seqlens, n_seqs);
   return hip_status(launch_repair(ra, stream));
 }
 
@@ -334,6 +341,7 @@ int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_
   ra.n_sink = n_sink;
   ra.n_recent = n_recent;
   ra.stats = stats;
+  ra.max_len = max_seq_len(cu_seqlens, n_seqs);
   return hip_status(launch_repair(ra, stream));
 }
 
@@ -394,6 +402,7 @@ int twinkv_score_evict(const void* keys, int dtype, int d, int n_heads, int n_se
   ea.T = bt.T;
   ea.n_sink = n_sink;
   ea.n_recent = n_recent;
+  ea.max_len = max_seq_len(cu_seqlens, n_seqs);
   return hip_status(launch_evict(ea, stream));
 }
 

@@ -4,49 +4,27 @@
 // Eviction: the score is s_i = -r_i / n (Eq. 3), the sink and recent regions score highest,
 // and the `budget` highest scores are retained; equal scores go to the later position first.
 // Ranking by the key  0 for protected positions, r_i + 1 otherwise  (ascending) gives the
-// same order.  The budget-th smallest key is found by an MSB-first 8-bit radix select with
-// LDS histograms; a block-wide scan in position order then keeps the last members equal to
-// that key.  Every pass streams the counts (4 bytes per token).
+// same order.  The budget-th smallest key is found by an MSB-first radix select (11/11/10-bit
+// digits, LDS histograms, 1024 or 256 threads); a block-wide scan in position order then keeps the
+// last members equal to that key.  Every pass streams the counts (4 bytes per token).
 //
 // Prevalence: for each threshold tau_k, the number of tokens whose best similarity outside
 // the window exceeds tau_k, i.e. that have at least one twin (Eq. 2).
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"
+#include "block_select.h"
 
 namespace twinkv {
 namespace {
 
-constexpr int kEvThreads = 256;
+constexpr int kEvThreads = 256;  // prevalence
 
-// Exclusive prefix sum over the block; `total` receives the block sum.
-__device__ inline int ev_exclusive_scan(int v, int* s_wave, int& total) {
-  const int lane = threadIdx.x & 63;
-  const int wv = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) s_wave[wv] = x;
-  __syncthreads();
-  int base = 0;
-  total = 0;
-#pragma unroll
-  for (int k = 0; k < kEvThreads / 64; ++k) {
-    const int t = s_wave[k];
-    base += (k < wv) ? t : 0;
-    total += t;
-  }
-  __syncthreads();
-  return base + x - v;
-}
-
-__global__ __launch_bounds__(kEvThreads) void evict_kernel(EvictArgs a) {
-  __shared__ int s_wave[kEvThreads / 64];
-  __shared__ int s_hist[256];
-  __shared__ int s_digit, s_before;
+template <int NT>
+__global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
+  __shared__ int s_wave[NT / 64];
+  __shared__ int s_hist[kSelBins];
+  __shared__ int s_pick[2];
 
   const int q = blockIdx.x;
   const int h = q / a.n_seqs;
@@ -68,42 +46,24 @@ __global__ __launch_bounds__(kEvThreads) void evict_kernel(EvictArgs a) {
   int take_eq = 0;
   const bool cut = budget > 0 && budget < len;
   if (cut) {
-    uint32_t prefix = 0, mask = 0;
-    int kk = budget;  // 1-based rank still to find among keys matching `prefix`
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      s_hist[tid] = 0;
-      __syncthreads();
-      for (int t = tid; t < len; t += kEvThreads) {
-        const uint32_t key = key_of(t);
-        if ((key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255u], 1);
-      }
-      __syncthreads();
-      const int hcount = s_hist[tid];
-      int dummy;
-      const int before = ev_exclusive_scan(hcount, s_wave, dummy);
-      if (before < kk && kk <= before + hcount) {
-        s_digit = tid;
-        s_before = before;
-      }
-      __syncthreads();
-      kk -= s_before;
-      prefix |= (uint32_t)s_digit << shift;
-      mask |= 0xFFu << shift;
-      __syncthreads();
-    }
-    key_cut = prefix;
-    take_eq = kk;  // members equal to key_cut still to keep: the last ones by position
+    key_cut = block_select<NT>(
+        len, budget,
+        [&](int t, uint32_t& key) {
+          key = key_of(t);
+          return true;
+        },
+        s_hist, s_wave, s_pick, take_eq);
   }
 
   // ---- final pass: contiguous ranges per thread so equal keys are ranked by position ----
-  const int span = (len + kEvThreads - 1) / kEvThreads;
+  const int span = (len + NT - 1) / NT;
   const int t0 = min(len, tid * span);
   const int t1 = min(len, t0 + span);
   int eq_here = 0;
   if (cut)
     for (int t = t0; t < t1; ++t) eq_here += key_of(t) == key_cut;
   int total_eq;
-  int eq_rank = ev_exclusive_scan(eq_here, s_wave, total_eq);
+  int eq_rank = sel_exclusive_scan<NT>(eq_here, s_wave, total_eq);
   const float inv_n = len > 0 ? 1.0f / (float)len : 0.0f;
   for (int t = t0; t < t1; ++t) {
     uint8_t keep;
@@ -160,7 +120,10 @@ __global__ __launch_bounds__(kEvThreads) void prevalence_kernel(PrevalenceArgs a
 int launch_evict(const EvictArgs& a, void* stream) {
   const int64_t P = (int64_t)a.n_heads * a.n_seqs;
   if (P == 0) return hipSuccess;
-  hipLaunchKernelGGL(evict_kernel, dim3((unsigned)P), dim3(kEvThreads), 0, (hipStream_t)stream, a);
+  if (a.max_len > 4096)
+    hipLaunchKernelGGL(evict_kernel<1024>, dim3((unsigned)P), dim3(1024), 0, (hipStream_t)stream, a);
+  else
+    hipLaunchKernelGGL(evict_kernel<256>, dim3((unsigned)P), dim3(256), 0, (hipStream_t)stream, a);
   return hipGetLastError();
 }
 

@@ -106,6 +106,7 @@ struct RepairArgs {
   int64_t T;
   float tau;
   int n_sink, n_recent;
+  int max_len;               // longest sequence (picks the workgroup size)
   int32_t* stats;            // [n_heads * n_seqs][4]
 };
 // K3: orphan / donor classification, radix selection of the m most severe, swap.
@@ -121,6 +122,7 @@ struct EvictArgs {
   int n_heads, n_seqs;
   int64_t T;
   int n_sink, n_recent;
+  int max_len;               // longest sequence (picks the workgroup size)
 };
 // K4a: the standalone scorer's retained set (the budget highest Eq. 3 scores).
 int launch_evict(const EvictArgs& a, void* stream);
