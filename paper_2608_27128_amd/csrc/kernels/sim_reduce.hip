@@ -56,6 +56,7 @@ struct Cfg {
   static constexpr int LOADS_PER_WAVE = TN * PPC / (NWAVES * 64);  // 1-KB direct loads
   static constexpr int VALU_PER_MFMA = (48 + KSTEPS - 1) / KSTEPS;
   static_assert((TN * PPC) % (NWAVES * 64) == 0, "tile copy must divide evenly");
+  static_assert(TN % 64 == 0, "the column tables move in 64-column (256-byte) pieces");
   static_assert(2 * (KEY_BYTES + TN * 8) + RETIRED <= 160 * 1024 / WG_PER_CU,
                 "LDS of WG_PER_CU workgroups must fit one CU");
 };
@@ -628,7 +629,7 @@ hipError_t run(const SimArgs& a, hipStream_t st) {
 #define TWINKV_CFG_BF16_128 128, false, 3, 4, 4, 2
 #endif
 #ifndef TWINKV_CFG_BF16_64
-#define TWINKV_CFG_BF16_64 64, false, 4, 4, 4, 2
+#define TWINKV_CFG_BF16_64 64, false, 4, 4, 2, 2
 #endif
 #ifndef TWINKV_CFG_F32_64
 #define TWINKV_CFG_F32_64 64, true, 1, 4, 4, 2
