@@ -14,6 +14,8 @@ for KV Cache Eviction via Pairwise Key Redundancy"):
                          and the retained set of the highest scores with the sink and
                          recent regions at the maximum score
   * Sec. 2 (Fig. 1b)     prevalence: how many tokens have at least one twin, per threshold
+  * Sec. 3.1             the compacted cache: only the keys and values at the retained
+                         positions survive eviction, gathered in position order
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library:
@@ -34,6 +36,10 @@ Readings where the paper is silent (each is exercised by a pin test):
       among equal scores the later position is retained first (recency).
   R20 the protected regions take the maximum score, so with K >= |P| they are all kept;
       with K < |P| the same order (later position first) decides among them.
+  R21 compaction writes the kept rows of each problem in ascending position order into
+      `capacity` reserved rows; rows past the kept count are zero with position -1, and
+      a problem that keeps more positions than it has rows is an error (status 1) whose
+      rows are all zero with position -1.
 Indices are 0-based positions within a sequence (the paper's 1-based positions only
 enter through |i-j| and region sizes, which the shift does not change).
 
@@ -48,7 +54,7 @@ __all__ = [
     "decode_keys", "normalise", "similarity_rows", "window_domain", "best_twin",
     "nn_scores", "classify", "rank_severity", "repair", "repair_problem",
     "protected_mask", "twin_counts", "redundancy_scores", "evict_by_score",
-    "score_evict_problem", "prevalence",
+    "score_evict_problem", "prevalence", "compact_problem", "compact",
 ]
 
 # Rows of the similarity matrix are evaluated in independent groups so that an
@@ -290,3 +296,60 @@ def prevalence(best_all: np.ndarray, taus) -> np.ndarray:
     token without any candidate (best = -1, reading R2) has none for tau >= -1."""
     b = np.asarray(best_all, dtype=np.float64)
     return np.array([int(np.sum(b > float(t))) for t in taus], dtype=np.int64)
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.1: the compacted cache
+# ----------------------------------------------------------------------------
+def compact_problem(keys: np.ndarray, values: np.ndarray | None, retained: np.ndarray,
+                    capacity: int) -> dict:
+    """One (sequence, layer, KV head) problem: eviction keeps only the keys and values at the
+    retained positions (Sec. 3.1).  Rows are copied bit for bit (any element dtype), in
+    ascending position order, into `capacity` rows (reading R21)."""
+    keys = np.asarray(keys)
+    keep = np.flatnonzero(np.asarray(retained) != 0)
+    n_keep = len(keep)
+    if capacity < 0:
+        raise ValueError("capacity must be >= 0")
+    ok = n_keep <= capacity
+    k_out = np.zeros((capacity,) + keys.shape[1:], dtype=keys.dtype)
+    v_out = None if values is None else np.zeros((capacity,) + np.asarray(values).shape[1:],
+                                                 dtype=np.asarray(values).dtype)
+    pos = np.full(capacity, -1, dtype=np.int64)
+    if ok:
+        k_out[:n_keep] = keys[keep]
+        if values is not None:
+            v_out[:n_keep] = np.asarray(values)[keep]
+        pos[:n_keep] = keep
+    return {"keys": k_out, "values": v_out, "pos": pos,
+            "stats": np.array([n_keep, capacity, 0 if ok else 1, 0], dtype=np.int64)}
+
+
+def compact(keys: np.ndarray, values: np.ndarray | None, retained: np.ndarray,
+            cu_seqlens, capacity) -> dict:
+    """A batch [n_heads][T][...] of ragged sequences: problem (h, s) goes to rows
+    [c_s, c_s + capacity[s]) of head h's block of sum(capacity) rows, c_s = sum of the
+    capacities before s."""
+    keys = np.asarray(keys)
+    H = keys.shape[0]
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    cap = np.asarray(capacity, dtype=np.int64)
+    n_seqs = len(cu) - 1
+    c0 = np.concatenate([[0], np.cumsum(cap)])
+    C = int(c0[-1])
+    k_out = np.zeros((H, C) + keys.shape[2:], dtype=keys.dtype)
+    v_out = None if values is None else np.zeros((H, C) + np.asarray(values).shape[2:],
+                                                 dtype=np.asarray(values).dtype)
+    pos = np.full((H, C), -1, dtype=np.int64)
+    stats = np.zeros((H * n_seqs, 4), dtype=np.int64)
+    for h in range(H):
+        for s in range(n_seqs):
+            a, e = int(cu[s]), int(cu[s + 1])
+            r = compact_problem(keys[h, a:e], None if values is None else np.asarray(values)[h, a:e],
+                                np.asarray(retained)[h, a:e], int(cap[s]))
+            k_out[h, c0[s]:c0[s + 1]] = r["keys"]
+            if values is not None:
+                v_out[h, c0[s]:c0[s + 1]] = r["values"]
+            pos[h, c0[s]:c0[s + 1]] = r["pos"]
+            stats[h * n_seqs + s] = r["stats"]
+    return {"keys": k_out, "values": v_out, "pos": pos, "stats": stats}

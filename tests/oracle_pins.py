@@ -374,6 +374,50 @@ def pin_prevalence_golden(o):
     np.testing.assert_array_equal(o.prevalence(np.asarray(fx["best"]), fx["taus"]), fx["counts"])
 
 
+# ----------------------------------------------------------------------------
+# Sec. 3.1: the compacted cache
+# ----------------------------------------------------------------------------
+def pin_compact_golden(o):
+    fx = _load("compact.json")
+    H, T = len(fx["retained"]), fx["cu_seqlens"][-1]
+    t = np.arange(T)
+    keys = np.stack([np.stack([10 * h + t, -(10 * h + t)], axis=1) for h in range(H)]).astype(np.int32)
+    vals = np.stack([np.stack([100 + 10 * h + t, 200 + 10 * h + t], axis=1)
+                     for h in range(H)]).astype(np.int32)
+    r = o.compact(keys, vals, np.asarray(fx["retained"], dtype=np.uint8), fx["cu_seqlens"],
+                  fx["capacity"])
+    np.testing.assert_array_equal(r["keys"], fx["keys_out"])
+    np.testing.assert_array_equal(r["values"], fx["values_out"])
+    np.testing.assert_array_equal(r["pos"], fx["pos"])
+    np.testing.assert_array_equal(r["stats"], fx["stats"])
+
+
+def pin_compact_invariants(o):
+    """The rows of a problem are exactly its kept rows, each once, in position order; the
+    rest is zero with position -1; bytes are copied unchanged (NaN payloads included)."""
+    rng = np.random.default_rng(17)
+    for trial in range(100):
+        n = int(rng.integers(0, 30))
+        d = int(rng.integers(1, 5))
+        bits = rng.integers(0, 2 ** 16, (n, d)).astype(np.uint16)   # arbitrary bf16 patterns
+        vbits = rng.integers(0, 2 ** 16, (n, d)).astype(np.uint16)
+        keep = (rng.random(n) < rng.random()).astype(np.uint8)
+        cap = int(rng.integers(0, n + 3))
+        r = o.compact_problem(bits, vbits, keep, cap)
+        k = int(keep.sum())
+        assert r["stats"][0] == k and r["stats"][1] == cap
+        if k > cap:
+            assert r["stats"][2] == 1
+            assert not r["keys"].any() and not r["values"].any() and np.all(r["pos"] == -1)
+            continue
+        assert r["stats"][2] == 0
+        pos = r["pos"][:k]
+        assert np.all(np.diff(pos) > 0) and set(pos.tolist()) == set(np.flatnonzero(keep).tolist())
+        for row, p in enumerate(pos):
+            assert np.array_equal(r["keys"][row], bits[p]) and np.array_equal(r["values"][row], vbits[p])
+        assert not r["keys"][k:].any() and not r["values"][k:].any() and np.all(r["pos"][k:] == -1)
+
+
 ALL_PINS = [
     pin_closed_forms, pin_window_and_sentinel, pin_scale_invariance, pin_bf16_decode,
     pin_nonfinite_rejected, pin_repair_ranked, pin_oscillation, pin_repair_invariants,
@@ -381,4 +425,5 @@ ALL_PINS = [
     pin_budget_checked,
     pin_twin_counts_golden, pin_twin_counts_brute_force, pin_twin_counts_vs_best,
     pin_scores_eq3, pin_evict_golden, pin_evict_invariants, pin_prevalence_golden,
+    pin_compact_golden, pin_compact_invariants,
 ]

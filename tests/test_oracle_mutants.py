@@ -61,6 +61,16 @@ MUTANTS = {
                           "score = redundancy_scores(counts, n)"),
     "evict_budget_off_by_one": ("keep[order[:min(budget, n)]] = 1", "keep[order[:min(budget + 1, n)]] = 1"),
     "prevalence_ge": ("np.sum(b > float(t))", "np.sum(b >= float(t))"),
+    # Sec. 3.1 compaction
+    "compact_reversed": ("keep = np.flatnonzero(np.asarray(retained) != 0)",
+                         "keep = np.flatnonzero(np.asarray(retained) != 0)[::-1]"),
+    "compact_evicted_rows": ("keep = np.flatnonzero(np.asarray(retained) != 0)",
+                             "keep = np.flatnonzero(np.asarray(retained) == 0)"),
+    "compact_overflow_truncates": ("ok = n_keep <= capacity", "ok = True; keep = keep[:capacity]"),
+    "compact_values_from_keys": ("v_out[:n_keep] = np.asarray(values)[keep]", "v_out[:n_keep] = keys[keep]"),
+    "compact_pos_one_based": ("pos[:n_keep] = keep", "pos[:n_keep] = keep + 1"),
+    "compact_seq_offset_ignored": ("k_out[h, c0[s]:c0[s + 1]] = r[\"keys\"]",
+                                   "k_out[h, :cap[s]] = r[\"keys\"]"),
 }
 
 
