@@ -27,7 +27,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 SIM_SOURCE = os.path.join(ROOT, "paper_2608_27128_amd", "csrc", "kernels", "sim_reduce.hip")
+COMPACT_SOURCE = os.path.join(ROOT, "paper_2608_27128_amd", "csrc", "kernels", "compact.hip")
 
 
 def log(*a):
@@ -63,12 +65,14 @@ class HipEvents:
         self.hip.hipEventDestroy(e)
 
 
-def profiled_traffic(workload: str):
-    """HBM bytes per launch of the similarity kernel from the committed rocprofv3 summary
-    (FETCH_SIZE + WRITE_SIZE, calibrated against a copy of known size), or None when no
-    summary exists for this workload or the kernel source has changed since it was taken."""
+def profiled_traffic(workload: str, name: str = "repair_pass", kernel: str = "sim_reduce",
+                     source: str = SIM_SOURCE):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 summary
+    profiles/<name>_<workload>.md (FETCH_SIZE + WRITE_SIZE, calibrated against a copy of known
+    size), or None when no summary exists for this workload or the kernel source has changed
+    since it was taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"repair_pass_{workload}.md")
+    path = os.path.join(ROOT, "profiles", f"{name}_{workload}.md")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -76,12 +80,12 @@ def profiled_traffic(workload: str):
         if ":" in line and not line.startswith(("|", "#", "`")):
             k, _, v = line.partition(":")
             fields[k.strip()] = v.strip()
-    with open(SIM_SOURCE, "rb") as f:
+    with open(source, "rb") as f:
         digest = hashlib.sha256(f.read()).hexdigest()[:16]
-    if fields.get("workload") != workload or fields.get("sim_reduce_source_sha256_16") != digest:
+    if fields.get("workload") != workload or fields.get(f"{kernel}_source_sha256_16") != digest:
         return None
     try:
-        return float(fields["sim_reduce_traffic_bytes_per_launch"])
+        return float(fields[f"{kernel}_traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
@@ -125,6 +129,111 @@ def cpu_baseline(batch, target_s: float = 15.0) -> dict:
                       f"({len(done)} problems), {pairs:.3e} ordered pairs in {spent:.1f} s"}
 
 
+def compact_cpu_baseline(batch, values_of, s1, target_s: float = 10.0) -> dict:
+    """oracle.compact_problem on whole problems in (head, sequence) order for about target_s
+    seconds; algorithmic bytes as for the GPU kernel."""
+    import numpy as np
+    import oracle
+    H, S = batch.n_heads, batch.n_seqs
+    nbytes, spent, done = 0.0, 0.0, 0
+    row = batch.keys.shape[2] * batch.keys.itemsize
+    for q in range(H * S):
+        h, s = divmod(q, S)
+        a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
+        cap = int(batch.budget[s])
+        v = values_of(batch.keys[h, a:e])
+        t = time.perf_counter()
+        r = oracle.compact_problem(batch.keys[h, a:e], v, s1[h, a:e], cap)
+        spent += time.perf_counter() - t
+        kept = int(r["stats"][0])
+        nbytes += (e - a) + 4.0 * kept * row + 4.0 * cap
+        done += 1
+        if spent >= target_s:
+            break
+    return {"value": nbytes / spent / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle.compact_problem on {done} whole problems of {H * S} "
+                      f"(keys and values, {row}-byte rows), {nbytes / 1e9:.2f} GB in {spent:.1f} s"}
+
+
+def compact_bench(args, sp, batch, keys, ret, dev) -> int:
+    """KV compaction of the keys and values at S1 (Sec. 3.1), S1 produced by one untimed
+    repair pass.  Value vectors: the key bits XOR a fixed pattern (any bits are valid rows).
+    Algorithmic bytes per step: the mask once, every kept row of keys and values read and
+    written once, one int32 position per reserved row."""
+    import numpy as np
+    import torch
+    from paper_2608_27128_amd import binding
+    cu = batch.cu_seqlens
+    H, T = batch.retained.shape
+    rep = binding.repair(keys, ret, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent, cu,
+                         want_all=False)
+    s1 = rep["s1"]
+    ibits = torch.int16 if keys.dtype == torch.bfloat16 else torch.int32
+    pattern = 0x5A5A if ibits == torch.int16 else 0x5A5A5A5A
+    vals = (keys.view(ibits) ^ pattern).view(keys.dtype)
+    cap = np.asarray(batch.budget, dtype=np.int64)
+    ws = torch.empty((binding.workspace_bytes(binding.OP_COMPACT, 0, batch.d, H, cu),),
+                     dtype=torch.uint8, device=dev)
+
+    def step(outputs=None):
+        return binding.compact(keys, s1, cap, values=vals, cu_seqlens=cu, outputs=outputs,
+                               workspace=ws)
+    out = step()
+    for _ in range(args.warmup):
+        step(out)
+    torch.cuda.synchronize()
+    hev = HipEvents()
+    g0 = [hev.create() for _ in range(args.steps)]
+    g1 = [hev.create() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        binding.profile_sim_events(g0[k], g1[k])
+        step(out)
+    binding.profile_sim_events(None, None)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_per_step = 1000.0 * wall / args.steps
+    g_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in zip(g0, g1)]))
+    for e in g0 + g1:
+        hev.destroy(e)
+    stats = out["stats"].cpu().numpy()
+    assert (stats[:, 2] == 0).all(), "a problem kept more rows than its capacity"
+    kept = float(stats[:, 0].sum())
+    row = batch.d * (2 if batch.dtype == "bf16" else 4)
+    nbytes = float(H * T) + 4.0 * kept * row + 4.0 * H * float(cap.sum())
+    log(f"[bench] compact {args.steps} steps: {ms_per_step:.3f} ms/step; gather kernel "
+        f"{g_ms:.3f} ms; {kept:.0f} rows kept; {nbytes / 1e9:.3f} GB algorithmic")
+    achieved = nbytes / (g_ms * 1e-3) / 1e9
+    result = {
+        "metric": "KV compaction: algorithmic HBM bytes per second (keys and values at S1)",
+        "value": nbytes / (ms_per_step * 1e-3) / 1e9,
+        "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if batch.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": sp.name, "problems": int(sp.n_heads * sp.n_seqs), "d": int(batch.d),
+                   "rows_per_problem": int(cap[0]), "path": "compact", "parallelism": "none"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": profiled_traffic(sp.name, "compact", "compact", COMPACT_SOURCE),
+                     "kernel": "compact_gather_kernel", "kernel_ms": g_ms,
+                     "bytes_per_launch": nbytes},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample ...")
+        if batch.dtype == "bf16":
+            def values_of(k):
+                return k ^ np.uint16(pattern)
+        else:
+            def values_of(k):
+                return (k.view(np.uint32) ^ np.uint32(pattern)).view(np.float32)
+        result["cpu_baseline"] = compact_cpu_baseline(batch, values_of, s1.cpu().numpy(),
+                                                      min(args.cpu_seconds, 10.0))
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,10 +241,12 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="long_aniso_32k",
                     help="tiny | llama1b_8k | qwen4b_16k | long_aniso_32k | ragged_64x")
-    ap.add_argument("--path", default="repair", choices=["repair", "repair_s0", "scorer"],
+    ap.add_argument("--path", default="repair",
+                    choices=["repair", "repair_s0", "scorer", "compact"],
                     help="repair: the full repair pass (both reductions, the headline); "
                          "repair_s0: the repair pass against retained columns only; "
-                         "scorer: the standalone scorer (Eq. 2 counts, Eq. 3 eviction)")
+                         "scorer: the standalone scorer (Eq. 2 counts, Eq. 3 eviction); "
+                         "compact: KV compaction of the keys and values at S1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -190,6 +301,9 @@ def main() -> int:
     else:
         pairs = float(sp.n_heads * np.sum(lens * lens))  # ordered key pairs per step
     flops = 2.0 * batch.d * pairs                         # dense masked K K^T, per launch
+
+    if args.path == "compact":
+        return compact_bench(args, sp, batch, keys, ret, dev)
 
     if args.path in ("repair", "repair_s0"):
         want_all = args.path == "repair"

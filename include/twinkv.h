@@ -12,7 +12,9 @@
  *     pairs are swapped, so |S1| = |S0| = K exactly;
  *   - the standalone scorer (Sec. 3.2, Eq. 2-3): twin counts r_i, scores s_i = -r_i / n, and
  *     the retained set of the K highest scores with the sink / recent regions kept first;
- *   - the prevalence statistic of Sec. 2 (Fig. 1b): tokens with at least one twin.
+ *   - the prevalence statistic of Sec. 2 (Fig. 1b): tokens with at least one twin;
+ *   - KV compaction (Sec. 3.1): only the keys and values at the retained positions are kept
+ *     for generation, gathered here into a dense cache.
  *
  * Problems.  A batch holds n_heads (layer, KV head) pairs times n_seqs sequences.  Sequence s
  * owns global token positions [cu_seqlens[s], cu_seqlens[s+1]) and T = cu_seqlens[n_seqs].
@@ -62,6 +64,7 @@ extern "C" {
 #define TWINKV_OP_REPAIR_FROM_SCORES 2
 #define TWINKV_OP_TWIN_COUNTS        3
 #define TWINKV_OP_SCORE_EVICT        4
+#define TWINKV_OP_COMPACT            5
 
 /* Most thresholds twinkv_prevalence takes in one call. */
 #define TWINKV_MAX_TAUS 32
@@ -74,7 +77,7 @@ extern "C" {
 /*
  * Bytes of workspace `op` needs for this batch; negative (-TWINKV_E_*) on invalid arguments.
  * cu_seqlens (host, n_seqs + 1 entries, non-decreasing, cu_seqlens[0] = 0).
- * dtype and d are ignored for TWINKV_OP_REPAIR_FROM_SCORES.  twinkv_prevalence needs none.
+ * dtype and d are ignored for TWINKV_OP_REPAIR_FROM_SCORES and TWINKV_OP_COMPACT.
  */
 int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs,
                                const int64_t* cu_seqlens);
@@ -201,10 +204,42 @@ int twinkv_prevalence(const float* best_all, int n_heads, int n_seqs, const int6
                       void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
+ * KV compaction (Sec. 3.1): eviction keeps only the keys and values at the retained
+ * positions.  For every problem (h, s) the rows of its retained tokens are copied, bit for
+ * bit and in ascending position order, into the problem's `capacity[s]` reserved rows of a
+ * dense cache; the usual caller passes S1 from twinkv_repair (or the scorer's retained set)
+ * with capacity = the budget.
+ *
+ *   keys, values  [n_heads][T][d] bf16 or fp32 at (head_stride, token_stride) and
+ *                 (v_head_stride, v_token_stride) elements (see Memory); d must be 64 or
+ *                 128.  values may be NULL (keys only), and then values_out must be NULL.
+ *   retained      [n_heads][T] uint8, nonzero = keep.
+ *   capacity      (host) [n_seqs] int64, 0 <= capacity[s] <= length of sequence s: rows
+ *                 reserved for each problem of sequence s.
+ *   keys_out, values_out  [n_heads][C][d] dense, same dtype, 16-byte aligned,
+ *                 C = sum of capacity.  Problem (h, s) owns rows [c_s, c_s + capacity[s]) of
+ *                 head h, c_s = sum of capacity[s'] for s' < s.  Must not overlap the inputs.
+ *   pos_out       [n_heads][C] int32: the position in the sequence of each row's token; -1
+ *                 for unused rows.  Nullable.
+ *   stats         [n_heads * n_seqs][4] int32 = {retained positions, capacity, status, 0};
+ *                 status TWINKV_PROBLEM_BUDGET_MISMATCH when a problem retains more
+ *                 positions than its capacity (then all its rows are zero, positions -1).
+ *                 Reserved rows past the retained count are zero with position -1.
+ *   workspace     twinkv_workspace_bytes(TWINKV_OP_COMPACT, ...) bytes.
+ */
+int twinkv_compact(const void* keys, const void* values, int dtype, int d, int n_heads,
+                   int n_seqs, const int64_t* cu_seqlens, int64_t head_stride,
+                   int64_t token_stride, int64_t v_head_stride, int64_t v_token_stride,
+                   const uint8_t* retained, const int64_t* capacity, void* keys_out,
+                   void* values_out, int32_t* pos_out, int32_t* stats, void* workspace,
+                   int64_t workspace_bytes, void* stream);
+
+/*
  * Profiling hook.  For calls made afterwards from the calling thread, record the given
  * hipEvent_t handles on the call's stream immediately before and immediately after the
- * launch of the similarity kernel (the fused contraction + reductions), so its duration can
- * be read with hipEventElapsedTime.  The events stay owned by the caller; pass NULL, NULL to
+ * launch of the call's main kernel -- the similarity kernel (the fused contraction +
+ * reductions), or in twinkv_compact the row gather -- so its duration can be read with
+ * hipEventElapsedTime.  The events stay owned by the caller; pass NULL, NULL to
  * stop recording.
  */
 void twinkv_profile_sim_events(void* start_event, void* stop_event);

@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libtwinkv.so")
 
 TWINKV_OK = 0
 TWINKV_BF16, TWINKV_F32 = 0, 1
-OP_NN_SCORES, OP_REPAIR, OP_REPAIR_FROM_SCORES, OP_TWIN_COUNTS, OP_SCORE_EVICT = 0, 1, 2, 3, 4
+OP_NN_SCORES, OP_REPAIR, OP_REPAIR_FROM_SCORES, OP_TWIN_COUNTS, OP_SCORE_EVICT, OP_COMPACT = range(6)
 MAX_TAUS = 32
 PROBLEM_OK, PROBLEM_BUDGET_MISMATCH, PROBLEM_NONFINITE = 0, 1, 2
 
@@ -47,6 +47,8 @@ SIGNATURES = {
                                 _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_prevalence": (_I, [_VP, _I, _I, _PI64, ctypes.POINTER(ctypes.c_float), _I, _VP, _VP,
                                _I64, _VP]),
+    "twinkv_compact": (_I, [_VP, _VP, _I, _I, _I, _I, _PI64, _I64, _I64, _I64, _I64, _VP, _PI64,
+                            _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_status_string": (ctypes.c_char_p, [_I]),
     "twinkv_version": (_I, []),
     "twinkv_profile_sim_events": (None, [_VP, _VP]),
@@ -359,3 +361,55 @@ def prevalence(best_all, taus, cu_seqlens=None) -> "torch.Tensor":
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_prevalence", rc)
     return out
+
+
+def compact(keys, retained, capacity, values=None, cu_seqlens=None, *, want_pos: bool = True,
+            workspace=None, outputs: Optional[dict] = None) -> dict:
+    """KV compaction (Sec. 3.1): the rows of the retained positions of every problem, in
+    position order, in its ``capacity[s]`` reserved rows: keys (and values) (n_heads, C, d),
+    positions (n_heads, C) int32 (-1 on unused rows) and stats {kept, capacity, status, 0}.
+    ``values`` must have the dtype and shape of ``keys``.  ``outputs`` may pass back the dict
+    of an earlier call with the same shapes to reuse its buffers."""
+    torch = _torch()
+    keys, dt = _prep_keys(keys)
+    H, T, d = keys.shape
+    dev = keys.device
+    if values is not None:
+        if values.dim() == 2:
+            values = values.unsqueeze(0)
+        if values.dtype != keys.dtype or tuple(values.shape) != (H, T, d) or values.device != dev:
+            raise ValueError("values must match keys in dtype, shape and device")
+        if values.stride(2) != 1:
+            values = values.contiguous()
+    cu = _cu(cu_seqlens, T)
+    if cu[-1] != T:
+        raise ValueError("cu_seqlens[-1] must equal T")
+    n_seqs = len(cu) - 1
+    ret = _mask(retained, H, T, dev, "retained")
+    if ret is None:
+        raise ValueError("retained is required")
+    cap = np.broadcast_to(np.asarray(capacity, dtype=np.int64), (n_seqs,)).copy()
+    C = int(cap.sum())
+    if outputs is None:
+        out = {
+            "keys": torch.empty((H, C, d), dtype=keys.dtype, device=dev),
+            "values": torch.empty((H, C, d), dtype=keys.dtype, device=dev) if values is not None else None,
+            "pos": torch.empty((H, C), dtype=torch.int32, device=dev) if want_pos else None,
+            "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
+        }
+    else:
+        out = dict(outputs)
+        out.setdefault("values", None)
+        out.setdefault("pos", None)
+    nbytes = workspace_bytes(OP_COMPACT, dt, d, H, cu)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
+        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    vs = (values.stride(0), values.stride(1)) if values is not None else (0, 0)
+    rc = lib().twinkv_compact(
+        keys.data_ptr(), _ptr(values), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0),
+        keys.stride(1), vs[0], vs[1], ret.data_ptr(), _i64_array(cap), out["keys"].data_ptr(),
+        _ptr(out["values"]), _ptr(out["pos"]), out["stats"].data_ptr(), ws.data_ptr(), ws.numel(),
+        _stream(dev))
+    if rc != TWINKV_OK:
+        raise TwinKVError("twinkv_compact", rc)
+    return {k: v for k, v in out.items() if v is not None}

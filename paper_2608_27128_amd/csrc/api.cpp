@@ -1,6 +1,7 @@
 // Host layer of the C ABI declared in include/twinkv.h: argument validation (pure host code,
 // done before anything is enqueued), workspace layout, the per-sequence schedule table and
-// the kernel launches (K1a partition, K1b key preparation, K2 similarity, K3 repair).
+// the kernel launches (K1a partition, K1b key preparation, K2 similarity, K3 repair, K4 scorer
+// eviction and prevalence, K5 KV compaction).
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -45,9 +46,28 @@ int check_batch(int n_heads, int n_seqs, const int64_t* cu, Batch& bt) {
   return TWINKV_OK;
 }
 
-Layout layout_for(int op, int dtype, int d, const Batch& bt) {
+// Chunks of the compaction's chunk list: ceil(len / kCompactChunk), at least 1 per sequence.
+int64_t compact_chunks(const int64_t* cu, int n_seqs) {
+  int64_t n = 0;
+  for (int s = 0; s < n_seqs; ++s)
+    n += std::max<int64_t>(1, (cu[s + 1] - cu[s] + kCompactChunk - 1) / kCompactChunk);
+  return n;
+}
+
+Layout layout_for(int op, int dtype, int d, const Batch& bt, const int64_t* cu = nullptr) {
   Layout L;
   size_t off = 0;
+  if (op == TWINKV_OP_COMPACT) {
+    const int64_t nch = compact_chunks(cu, bt.n_seqs);
+    L.seqtab = off;
+    off = align_up(off + sizeof(CompactSeq) * (size_t)bt.n_seqs);
+    L.chunk_seq = off;
+    off = align_up(off + 4 * (size_t)nch);
+    L.chunk_cnt = off;
+    off = align_up(off + 4 * (size_t)nch * (size_t)bt.n_heads);
+    L.total = off + kAlign;
+    return L;
+  }
   L.seqtab = off;
   off = align_up(off + sizeof(SeqInfo) * (size_t)bt.n_seqs);
   if (op != TWINKV_OP_REPAIR_FROM_SCORES) {
@@ -133,7 +153,8 @@ int max_seq_len(const int64_t* cu, int n_seqs) {
   return (int)m;
 }
 
-// Events recorded around the similarity kernel (twinkv_profile_sim_events), per thread.
+// Events recorded around the similarity kernel, or the compaction's gather kernel
+// (twinkv_profile_sim_events), per thread.
 thread_local hipEvent_t g_sim_start = nullptr;
 thread_local hipEvent_t g_sim_stop = nullptr;
 
@@ -222,16 +243,16 @@ extern "C" {
 int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs,
                                const int64_t* cu_seqlens) {
   if (op != TWINKV_OP_NN_SCORES && op != TWINKV_OP_REPAIR && op != TWINKV_OP_REPAIR_FROM_SCORES &&
-      op != TWINKV_OP_TWIN_COUNTS && op != TWINKV_OP_SCORE_EVICT)
+      op != TWINKV_OP_TWIN_COUNTS && op != TWINKV_OP_SCORE_EVICT && op != TWINKV_OP_COMPACT)
     return -TWINKV_E_ARG;
-  if (op != TWINKV_OP_REPAIR_FROM_SCORES) {
+  if (op != TWINKV_OP_REPAIR_FROM_SCORES && op != TWINKV_OP_COMPACT) {
     if (dtype != TWINKV_BF16 && dtype != TWINKV_F32) return -TWINKV_E_UNSUPPORTED;
     if (d != 64 && d != 128) return -TWINKV_E_UNSUPPORTED;
   }
   Batch bt;
   const int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
   if (rc != TWINKV_OK) return -rc;
-  return (int64_t)layout_for(op, dtype, d, bt).total;
+  return (int64_t)layout_for(op, dtype, d, bt, cu_seqlens).total;
 }
 
 int twinkv_nn_scores(const void* keys, int dtype, int d, int n_heads, int n_seqs,
@@ -433,6 +454,95 @@ int twinkv_prevalence(const float* best_all, int n_heads, int n_seqs, const int6
   pa.n_taus = n_taus;
   for (int k = 0; k < kMaxTaus; ++k) pa.taus[k] = k < n_taus ? taus[k] : 0.0f;
   return hip_status(launch_prevalence(pa, stream));
+}
+
+int twinkv_compact(const void* keys, const void* values, int dtype, int d, int n_heads,
+                   int n_seqs, const int64_t* cu_seqlens, int64_t head_stride,
+                   int64_t token_stride, int64_t v_head_stride, int64_t v_token_stride,
+                   const uint8_t* retained, const int64_t* capacity, void* keys_out,
+                   void* values_out, int32_t* pos_out, int32_t* stats, void* workspace,
+                   int64_t workspace_bytes, void* stream) {
+  int rc = check_keys(keys, dtype, d, head_stride, token_stride, 0);
+  if (rc != TWINKV_OK) return rc;
+  if (retained == nullptr || capacity == nullptr || keys_out == nullptr || stats == nullptr)
+    return TWINKV_E_NULL;
+  if ((values == nullptr) != (values_out == nullptr)) return TWINKV_E_NULL;
+  if (values != nullptr) {
+    rc = check_keys(values, dtype, d, v_head_stride, v_token_stride, 0);
+    if (rc != TWINKV_OK) return rc;
+  }
+  if (reinterpret_cast<uintptr_t>(keys_out) % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(values_out) % 16 != 0)
+    return TWINKV_E_ARG;
+  Batch bt;
+  rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  int64_t C = 0;
+  for (int s = 0; s < n_seqs; ++s) {
+    if (capacity[s] < 0 || capacity[s] > cu_seqlens[s + 1] - cu_seqlens[s]) return TWINKV_E_ARG;
+    C += capacity[s];
+  }
+  const int64_t nch = compact_chunks(cu_seqlens, n_seqs);
+  if ((int64_t)n_heads * nch > (int64_t)INT32_MAX) return TWINKV_E_ARG;
+  const Layout L = layout_for(TWINKV_OP_COMPACT, dtype, d, bt, cu_seqlens);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+
+  // sequence table and chunk list, one host-to-device copy
+  const size_t tab_bytes = L.chunk_cnt - L.seqtab;
+  std::vector<char> host(tab_bytes, 0);
+  CompactSeq* tab = reinterpret_cast<CompactSeq*>(host.data());
+  int32_t* cseq = reinterpret_cast<int32_t*>(host.data() + (L.chunk_seq - L.seqtab));
+  int64_t out = 0, ck = 0;
+  for (int s = 0; s < n_seqs; ++s) {
+    const int64_t len = cu_seqlens[s + 1] - cu_seqlens[s];
+    const int64_t nc = std::max<int64_t>(1, (len + kCompactChunk - 1) / kCompactChunk);
+    tab[s].start = (int32_t)cu_seqlens[s];
+    tab[s].len = (int32_t)len;
+    tab[s].cap = (int32_t)capacity[s];
+    tab[s].out_start = (int32_t)out;
+    tab[s].chunk0 = (int32_t)ck;
+    tab[s].nchunks = (int32_t)nc;
+    for (int64_t c = 0; c < nc; ++c) cseq[ck + c] = s;
+    out += capacity[s];
+    ck += nc;
+  }
+  if (hipMemcpyAsync(ws + L.seqtab, host.data(), tab_bytes, hipMemcpyHostToDevice,
+                     (hipStream_t)stream) != hipSuccess)
+    return TWINKV_E_HIP;
+
+  const int64_t esz = dtype == TWINKV_F32 ? 4 : 2;
+  CompactArgs a;
+  a.keys = static_cast<const char*>(keys);
+  a.values = static_cast<const char*>(values);
+  a.head_stride = head_stride * esz;
+  a.token_stride = token_stride * esz;
+  a.v_head_stride = v_head_stride * esz;
+  a.v_token_stride = v_token_stride * esz;
+  a.row_bytes = (int)(d * esz);
+  int lp = 0;
+  while ((16 << lp) < a.row_bytes) ++lp;
+  a.log2_pieces = lp;
+  a.retained = retained;
+  a.seqs = reinterpret_cast<const CompactSeq*>(ws + L.seqtab);
+  a.chunk_seq = reinterpret_cast<const int32_t*>(ws + L.chunk_seq);
+  a.chunk_cnt = reinterpret_cast<int32_t*>(ws + L.chunk_cnt);
+  a.keys_out = static_cast<char*>(keys_out);
+  a.values_out = static_cast<char*>(values_out);
+  a.pos_out = pos_out;
+  a.stats = stats;
+  a.n_heads = n_heads;
+  a.n_seqs = n_seqs;
+  a.n_chunks = (int)nch;
+  a.T = bt.T;
+  a.C = C;
+  int e = launch_compact_count(a, stream);
+  if (e) return hip_status(e);
+  if (g_sim_start && hipEventRecord(g_sim_start, (hipStream_t)stream) != hipSuccess) return TWINKV_E_HIP;
+  e = launch_compact_gather(a, stream);
+  if (e) return hip_status(e);
+  if (g_sim_stop && hipEventRecord(g_sim_stop, (hipStream_t)stream) != hipSuccess) return TWINKV_E_HIP;
+  return TWINKV_OK;
 }
 
 const char* twinkv_status_string(int status) {

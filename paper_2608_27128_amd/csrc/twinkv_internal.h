@@ -42,7 +42,7 @@ constexpr int kFlagNonfinite = 1;
 // Workspace layout shared by the size query and the launchers.
 struct Layout {
   size_t seqtab = 0, rinv = 0, pcol = 0, rcol = 0, prank = 0, pmeta = 0, hilo = 0, pkeys = 0,
-         bbuf = 0;
+         bbuf = 0, chunk_seq = 0, chunk_cnt = 0;
   size_t total = 0;
 };
 
@@ -139,5 +139,43 @@ struct PrevalenceArgs {
 };
 // K4b: tokens with at least one twin per threshold (best_all > tau).
 int launch_prevalence(const PrevalenceArgs& a, void* stream);
+
+// KV compaction: positions per chunk of the retained mask, one workgroup per (head, chunk).
+#ifndef TWINKV_COMPACT_CHUNK
+#define TWINKV_COMPACT_CHUNK 2048
+#endif
+constexpr int kCompactChunk = TWINKV_COMPACT_CHUNK;
+struct CompactSeq {
+  int32_t start;      // first global token of the sequence
+  int32_t len;        // tokens
+  int32_t cap;        // reserved output rows per problem of this sequence (<= len)
+  int32_t out_start;  // first reserved row inside a head's block of C rows
+  int32_t chunk0;     // first chunk of the sequence in the chunk list
+  int32_t nchunks;    // chunks of the sequence (at least 1, so every problem reports stats)
+  int32_t pad[2];
+};
+struct CompactArgs {
+  const char* keys;          // byte addresses; rows of row_bytes at the given byte strides
+  const char* values;        // nullable
+  int64_t head_stride, token_stride;      // bytes
+  int64_t v_head_stride, v_token_stride;  // bytes
+  int row_bytes;             // d * element size, a multiple of 16
+  int log2_pieces;           // log2(row_bytes / 16)
+  const uint8_t* retained;   // [n_heads][T]
+  const CompactSeq* seqs;    // [n_seqs]
+  const int32_t* chunk_seq;  // [n_chunks]: sequence of each chunk
+  int32_t* chunk_cnt;        // [n_heads][n_chunks]: kept positions per chunk (workspace)
+  char* keys_out;            // [n_heads][C] rows
+  char* values_out;          // nullable, like keys_out
+  int32_t* pos_out;          // nullable [n_heads][C]
+  int32_t* stats;            // [n_heads * n_seqs][4]
+  int n_heads, n_seqs, n_chunks;
+  int64_t T, C;
+};
+// K5a: kept positions per (head, chunk) into chunk_cnt.
+int launch_compact_count(const CompactArgs& a, void* stream);
+// K5b (after K5a): the kept rows of every problem gathered in position order into its
+// reserved rows, unused rows zeroed, stats written.
+int launch_compact_gather(const CompactArgs& a, void* stream);
 
 }  // namespace twinkv

@@ -60,6 +60,12 @@ def test_workspace_bytes():
     tc = L.twinkv_workspace_bytes(3, 0, 64, 8, 1, cu_arr([0, 1000]))
     se = L.twinkv_workspace_bytes(4, 0, 64, 8, 1, cu_arr([0, 1000]))
     assert tc == bf and se > tc           # the scorer adds the count buffer
+    # compaction: the sequence table, the chunk list and one count per (head, chunk)
+    c1 = L.twinkv_workspace_bytes(5, 0, 0, 8, 1, cu_arr([0, 2048]))
+    c2 = L.twinkv_workspace_bytes(5, 0, 0, 8, 1, cu_arr([0, 2049]))
+    c3 = L.twinkv_workspace_bytes(5, 0, 0, 8, 3, cu_arr([0, 0, 0, 0]))
+    assert 0 < c1 <= c2 and c3 > 0
+    assert L.twinkv_workspace_bytes(5, 0, 0, 8, 1, cu_arr([0, 2048 * 300])) > c1 + 4 * 8 * 290
     assert L.twinkv_workspace_bytes(0, 0, 64, 0, 1, cu_arr([0, 10])) == -E_ARG
     assert L.twinkv_workspace_bytes(0, 0, 64, 8, 2, cu_arr([0, 10, 5])) == -E_ARG
     assert L.twinkv_workspace_bytes(0, 0, 64, 8, 1, cu_arr([3, 10])) == -E_ARG
@@ -167,6 +173,34 @@ def test_prevalence_validation():
     assert call(n=0) == E_ARG
     assert call(n=33) == E_ARG                  # more thresholds than one call takes
     assert call(wsb=0) == E_WS
+
+
+def test_compact_validation():
+    L = binding.lib()
+
+    def call(keys=FAKE, vals=FAKE, dtype=0, d=64, cu=(0, 100), hs=6400, ts=64, vhs=6400, vts=64,
+             ret=FAKE, cap=(50,), kout=FAKE, vout=FAKE, pos=None, stats=FAKE, wsb=1 << 40):
+        c = cu_arr(list(cap)) if cap is not None else None
+        return L.twinkv_compact(keys, vals, dtype, d, 2, len(cu) - 1, cu_arr(list(cu)), hs, ts,
+                                vhs, vts, ret, c, kout, vout, pos, stats, FAKE, wsb, None)
+    assert call(keys=None) == E_NULL
+    assert call(ret=None) == E_NULL
+    assert call(cap=None) == E_NULL
+    assert call(kout=None) == E_NULL
+    assert call(stats=None) == E_NULL
+    assert call(vout=None) == E_NULL            # values without values_out
+    assert call(vals=None) == E_NULL            # values_out without values
+    assert call(d=96) == E_UNSUP
+    assert call(dtype=3) == E_UNSUP
+    assert call(cap=(101,)) == E_ARG            # more rows than the sequence has tokens
+    assert call(cap=(-1,)) == E_ARG
+    assert call(ts=63) == E_ARG
+    assert call(vts=60) == E_ARG                # value rows not 16-byte aligned
+    assert call(kout=FAKE + 8) == E_ARG
+    assert call(vout=FAKE + 4) == E_ARG
+    assert call(keys=FAKE + 2) == E_ARG
+    assert call(cu=(0, 60, 50), cap=(1, 1)) == E_ARG
+    assert call(wsb=16) == E_WS
 
 
 def test_binding_refuses_host_tensors():
