@@ -452,6 +452,10 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     }
   };
 
+  // A wave whose rows all lie past the end of the sequence (in the last row block of a
+  // sequence) only takes its share of the tile loads; its SIMD's MFMA pipe is left to the
+  // other workgroup's wave.
+  const bool active = wrow0 < len;
   if (ntiles > 0) issue_tile(0, 0);
 #pragma unroll 1
   for (int tile = 0; tile < ntiles; ++tile) {
@@ -471,8 +475,10 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       retire();
     }
     const uint32_t keep = __builtin_amdgcn_readfirstlane(keep_bits(c0));
-    if (buf == 0) sweep_tile(std::integral_constant<int, 0>{}, c0, keep);
-    else sweep_tile(std::integral_constant<int, 1>{}, c0, keep);
+    if (active) {
+      if (buf == 0) sweep_tile(std::integral_constant<int, 0>{}, c0, keep);
+      else sweep_tile(std::integral_constant<int, 1>{}, c0, keep);
+    }
   }
   reduce_into(pacc, prv, pgc, NSUB - 1, pmask);
   if (!retired_done) retire();          // no evicted columns were swept
@@ -532,7 +538,7 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       if (gc < nchunks) masked_chunk(gc, rs, cs);
   };
   // evicted group: the live registers
-  if (a.want_all) {
+  if (active && a.want_all) {
     masked_range(ce_lo, ce_hi, run, cid);
     if (pad_e >= 0 && !(pad_e >= ce_lo && pad_e <= ce_hi)) masked_range(pad_e, pad_e, run, cid);
   }
@@ -546,8 +552,10 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       rr[s] = v.x;
       rcid[s] = (int)v.y;
     }
-    masked_range(cr_lo, cr_hi, rr, rcid);
-    if (pad_r >= 0 && !(pad_r >= cr_lo && pad_r <= cr_hi)) masked_range(pad_r, pad_r, rr, rcid);
+    if (active) {
+      masked_range(cr_lo, cr_hi, rr, rcid);
+      if (pad_r >= 0 && !(pad_r >= cr_lo && pad_r <= cr_hi)) masked_range(pad_r, pad_r, rr, rcid);
+    }
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) retired[s * 64 + lane] = make_uint2(rr[s], (uint32_t)rcid[s]);
   }
