@@ -119,14 +119,18 @@ int check_keys(const void* keys, int dtype, int d, int64_t head_stride, int64_t 
 
 // Builds the per-sequence table (schedule of similarity row blocks, longest first).
 std::vector<SeqInfo> seq_table(const int64_t* cu, int n_seqs, const int64_t* budget, int rows_per_block,
-                               int& total_tiles) {
+                               int& total_tiles, int prep_tokens = 0, int64_t* prep_blocks = nullptr) {
   std::vector<SeqInfo> tab(n_seqs);
+  int64_t pb = 0;
   for (int s = 0; s < n_seqs; ++s) {
     tab[s].start = (int32_t)cu[s];
     tab[s].len = (int32_t)(cu[s + 1] - cu[s]);
     tab[s].budget = budget ? (int32_t)budget[s] : -1;
     tab[s].perm_off = (int32_t)(cu[s] + (int64_t)kPermPad * s);
+    tab[s].prep_blk0 = (int32_t)pb;
+    if (prep_tokens > 0) pb += (tab[s].len + prep_tokens - 1) / prep_tokens;
   }
+  if (prep_blocks) *prep_blocks = pb;
   std::vector<int> order(n_seqs);
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(),
@@ -138,7 +142,6 @@ std::vector<SeqInfo> seq_table(const int64_t* cu, int n_seqs, const int64_t* bud
     tab[r].sorted_seq = s;
     tab[r].tile_cum = cum;
     tab[r].nb = nb;
-    tab[r].pad = 0;
     cum += nb;
   }
   total_tiles = cum;
@@ -167,7 +170,10 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
                int32_t* counts = nullptr) {
   int total_tiles = 0;
   const int rpb = sim_rows_per_block(dtype, d);
-  std::vector<SeqInfo> tab = seq_table(cu, bt.n_seqs, budget, rpb, total_tiles);
+  int64_t prep_blocks = 0;
+  std::vector<SeqInfo> tab = seq_table(cu, bt.n_seqs, budget, rpb, total_tiles,
+                                       prepare_tokens_per_block(dtype, d), &prep_blocks);
+  if (prep_blocks > (int64_t)INT32_MAX) return TWINKV_E_ARG;
   const int64_t groups = bt.n_heads >= 8 ? 8LL * ((bt.n_heads + 7) / 8) : bt.n_heads;
   if (groups * total_tiles > (int64_t)INT32_MAX) return TWINKV_E_ARG;
 
@@ -188,11 +194,9 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
   int e = launch_partition(retained, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT, pcol, rcol, prank,
                            pmeta, status, stream);
   if (e) return hip_status(e);
-  int max_len = 0;
-  for (int s = 0; s < bt.n_seqs; ++s) max_len = std::max(max_len, (int)(cu[s + 1] - cu[s]));
   e = launch_prepare_keys(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, bt.PT,
-                          max_len, retained, prank, pmeta, dtab, bt.n_seqs, rinv, rcol, hilo, pkeys, status,
-                          stream);
+                          (int)prep_blocks, retained, prank, pmeta, dtab, bt.n_seqs, rinv, rcol,
+                          hilo, pkeys, status, stream);
   if (e) return hip_status(e);
 
   SimArgs a;

@@ -111,107 +111,129 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
   }
 }
 
-// LPT lanes cooperate on one key; each lane owns 16 contiguous bytes of it.  blockIdx.y is
-// the (head, sequence) problem, blockIdx.x a group of TPB of its tokens, so the problem's
-// table entries are uniform across the workgroup.
+// LPT lanes cooperate on one key; each lane owns 16 contiguous bytes of it.  A workgroup
+// takes kPrepIter groups of TPB consecutive tokens of one (head, sequence) problem, all their
+// loads issued before any is used.  blockIdx.y is the head; blockIdx.x runs over the
+// workgroups of all sequences (seqtab[s].prep_blk0 = the first one of sequence s), so no
+// workgroup is launched past the end of a short sequence.
+constexpr int kPrepIter = 4;
+
 template <int D, bool F32>
 __global__ __launch_bounds__(256) void prepare_keys_kernel(
     const uint8_t* __restrict__ keys, int64_t T, int64_t hs_bytes, int64_t ts_bytes, int64_t PT,
     const uint8_t* __restrict__ retained, const int32_t* __restrict__ prank,
     ProblemMeta* __restrict__ pmeta, const SeqInfo* __restrict__ seqtab, int n_seqs,
     float* __restrict__ rinv, float* __restrict__ rcol, uint16_t* __restrict__ hilo,
-    uint16_t* __restrict__ pkeys, int32_t* __restrict__ status, int q0) {
+    uint16_t* __restrict__ pkeys, int32_t* __restrict__ status, int h0) {
   constexpr int ESZ = F32 ? 4 : 2;
   constexpr int LPT = D * ESZ / 16;
   constexpr int TPB = 256 / LPT;
   constexpr int DCOL = F32 ? 2 * D : D;
   static_assert(LPT <= 64 && (64 % LPT) == 0, "a key must fit inside one wave");
-  const int q = q0 + (int)blockIdx.y;
-  const int64_t h = q / n_seqs;
-  const int s = q - (int)h * n_seqs;
+  const int64_t h = h0 + (int64_t)blockIdx.y;
+  const int bx = (int)blockIdx.x;
+  int lo = 0, hi = n_seqs - 1;  // the last sequence whose first workgroup is <= bx
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (seqtab[mid].prep_blk0 <= bx) lo = mid; else hi = mid - 1;
+  }
+  const int s = lo;
+  const int q = (int)h * n_seqs + s;
   const SeqInfo si = seqtab[s];
-  const int tl0 = blockIdx.x * TPB;
-  if (tl0 >= si.len) return;                 // sequences shorter than the longest
   const int sub = threadIdx.x % LPT;
-  const int tl = tl0 + threadIdx.x / LPT;
-  const bool valid = tl < si.len;
-  const int64_t tt = si.start + (valid ? tl : 0);
+  const int tfirst = (bx - si.prep_blk0) * (TPB * kPrepIter) + threadIdx.x / LPT;
   const int64_t base = h * PT + si.perm_off;
-  uint4 raw = make_uint4(0, 0, 0, 0);
-  if (valid) raw = *reinterpret_cast<const uint4*>(keys + h * hs_bytes + tt * ts_bytes + sub * 16);
-  const bool r = retained != nullptr && retained[h * T + tt] != 0;
-  const int pr = prank[base + (valid ? tl : 0)];
-  const int p = r ? pr : pmeta[q].ret_chunks * kChunk + ((valid ? tl : 0) - pr);
-  uint16_t* dst = pkeys + (base + p) * DCOL;
+  const int ret_cols = pmeta[q].ret_chunks * kChunk;
 
-  double ss = 0.0;
-  if constexpr (F32) {
-    float v[4] = {__uint_as_float(raw.x), __uint_as_float(raw.y), __uint_as_float(raw.z),
-                  __uint_as_float(raw.w)};
-    uint16_t hs[4], ls[4];
+  uint4 raw[kPrepIter];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      ss += (double)v[e] * (double)v[e];
-      hs[e] = bf16_rne(v[e]);
-      ls[e] = bf16_rne(v[e] - bf16_to_f32(hs[e]));  // v - hi is exact in fp32
-    }
-    if (valid) {
-      uint2 phi, plo;
-      phi.x = hs[0] | ((uint32_t)hs[1] << 16);
-      phi.y = hs[2] | ((uint32_t)hs[3] << 16);
-      plo.x = ls[0] | ((uint32_t)ls[1] << 16);
-      plo.y = ls[2] | ((uint32_t)ls[3] << 16);
-      uint16_t* row = hilo + (h * T + tt) * (2 * D) + sub * 4;
-      *reinterpret_cast<uint2*>(row) = phi;
-      *reinterpret_cast<uint2*>(row + D) = plo;
-      *reinterpret_cast<uint2*>(dst + sub * 4) = phi;
-      *reinterpret_cast<uint2*>(dst + D + sub * 4) = plo;
-    }
-  } else {
-    const uint32_t wds[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const double x0 = (double)__uint_as_float(wds[e] << 16);
-      const double x1 = (double)__uint_as_float(wds[e] & 0xFFFF0000u);
-      ss += x0 * x0 + x1 * x1;
-    }
-    if (valid) *reinterpret_cast<uint4*>(dst + sub * 8) = raw;
+  for (int it = 0; it < kPrepIter; ++it) {
+    const int tl = tfirst + it * TPB;
+    raw[it] = make_uint4(0, 0, 0, 0);
+    if (tl < si.len)
+      raw[it] = *reinterpret_cast<const uint4*>(keys + h * hs_bytes + (si.start + tl) * ts_bytes +
+                                                sub * 16);
   }
 #pragma unroll
-  for (int off = LPT / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, LPT);
-  if (valid && sub == 0) {
-    float rv;
-    const bool bad = !(ss < 1.0e300);                    // NaN or Inf in the key
-    if (bad) rv = __uint_as_float(0x7FC00000u);
-    else if (ss > 0.0) rv = (float)(1.0 / sqrt(ss));
-    else rv = 0.0f;                                       // zero key: similarity 0 to all
-    rinv[h * T + tt] = rv;
-    rcol[base + p] = rv;
-    if (bad) {
-      atomicOr(&pmeta[q].flags, kFlagNonfinite);
-      if (status) status[q] = 2;  // TWINKV_PROBLEM_NONFINITE
+  for (int it = 0; it < kPrepIter; ++it) {
+    const int tl = tfirst + it * TPB;
+    const bool valid = tl < si.len;
+    const int64_t tt = si.start + (valid ? tl : 0);
+    const bool r = retained != nullptr && retained[h * T + tt] != 0;
+    const int pr = prank[base + (valid ? tl : 0)];
+    const int p = r ? pr : ret_cols + ((valid ? tl : 0) - pr);
+    uint16_t* dst = pkeys + (base + p) * DCOL;
+
+    double ss = 0.0;
+    if constexpr (F32) {
+      float v[4] = {__uint_as_float(raw[it].x), __uint_as_float(raw[it].y),
+                    __uint_as_float(raw[it].z), __uint_as_float(raw[it].w)};
+      uint16_t hs[4], ls[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ss += (double)v[e] * (double)v[e];
+        hs[e] = bf16_rne(v[e]);
+        ls[e] = bf16_rne(v[e] - bf16_to_f32(hs[e]));  // v - hi is exact in fp32
+      }
+      if (valid) {
+        uint2 phi, plo;
+        phi.x = hs[0] | ((uint32_t)hs[1] << 16);
+        phi.y = hs[2] | ((uint32_t)hs[3] << 16);
+        plo.x = ls[0] | ((uint32_t)ls[1] << 16);
+        plo.y = ls[2] | ((uint32_t)ls[3] << 16);
+        uint16_t* row = hilo + (h * T + tt) * (2 * D) + sub * 4;
+        *reinterpret_cast<uint2*>(row) = phi;
+        *reinterpret_cast<uint2*>(row + D) = plo;
+        *reinterpret_cast<uint2*>(dst + sub * 4) = phi;
+        *reinterpret_cast<uint2*>(dst + D + sub * 4) = plo;
+      }
+    } else {
+      const uint32_t wds[4] = {raw[it].x, raw[it].y, raw[it].z, raw[it].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double x0 = (double)__uint_as_float(wds[e] << 16);
+        const double x1 = (double)__uint_as_float(wds[e] & 0xFFFF0000u);
+        ss += x0 * x0 + x1 * x1;
+      }
+      if (valid) *reinterpret_cast<uint4*>(dst + sub * 8) = raw[it];
+    }
+#pragma unroll
+    for (int off = LPT / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, LPT);
+    if (valid && sub == 0) {
+      float rv;
+      const bool bad = !(ss < 1.0e300);                    // NaN or Inf in the key
+      if (bad) rv = __uint_as_float(0x7FC00000u);
+      else if (ss > 0.0) rv = (float)(1.0 / sqrt(ss));
+      else rv = 0.0f;                                       // zero key: similarity 0 to all
+      rinv[h * T + tt] = rv;
+      rcol[base + p] = rv;
+      if (bad) {
+        atomicOr(&pmeta[q].flags, kFlagNonfinite);
+        if (status) status[q] = 2;  // TWINKV_PROBLEM_NONFINITE
+      }
     }
   }
 }
 
 template <int D, bool F32>
+constexpr int prep_tokens_per_block() {
+  return 256 / (D * (F32 ? 4 : 2) / 16) * kPrepIter;
+}
+
+template <int D, bool F32>
 hipError_t run_prepare(const void* keys, int n_heads, int64_t T, int64_t hs, int64_t ts,
-                       int64_t PT, int max_len, const uint8_t* retained, const int32_t* prank,
+                       int64_t PT, int total_blocks, const uint8_t* retained, const int32_t* prank,
                        ProblemMeta* pmeta, const SeqInfo* seqtab, int n_seqs, float* rinv,
                        float* rcol, uint16_t* hilo, uint16_t* pkeys, int32_t* status,
                        hipStream_t st) {
   constexpr int ESZ = F32 ? 4 : 2;
-  constexpr int LPT = D * ESZ / 16;
-  constexpr int TPB = 256 / LPT;
-  if (max_len == 0 || n_heads == 0) return hipSuccess;
-  const int64_t bx = (max_len + TPB - 1) / TPB;
-  const int64_t P = (int64_t)n_heads * n_seqs;
-  for (int64_t q0 = 0; q0 < P; q0 += 65535) {  // problems along y, in slices the grid holds
-    const int64_t by = P - q0 < 65535 ? P - q0 : 65535;
-    hipLaunchKernelGGL((prepare_keys_kernel<D, F32>), dim3((unsigned)bx, (unsigned)by),
+  if (total_blocks == 0 || n_heads == 0) return hipSuccess;
+  for (int h0 = 0; h0 < n_heads; h0 += 65535) {  // heads along y, in slices the grid holds
+    const int by = n_heads - h0 < 65535 ? n_heads - h0 : 65535;
+    hipLaunchKernelGGL((prepare_keys_kernel<D, F32>), dim3((unsigned)total_blocks, (unsigned)by),
                        dim3(256), 0, st, (const uint8_t*)keys, T, hs * ESZ, ts * ESZ, PT,
                        retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status,
-                       (int)q0);
+                       h0);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -231,24 +253,36 @@ int launch_partition(const uint8_t* retained, const SeqInfo* seqtab, int n_heads
   return hipGetLastError();
 }
 
+int prepare_tokens_per_block(int dtype, int d) {
+  if (dtype == 0 && d == 64) return prep_tokens_per_block<64, false>();
+  if (dtype == 0 && d == 128) return prep_tokens_per_block<128, false>();
+  if (dtype == 1 && d == 64) return prep_tokens_per_block<64, true>();
+  if (dtype == 1 && d == 128) return prep_tokens_per_block<128, true>();
+  return 0;
+}
+
 int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t T,
-                        int64_t head_stride, int64_t token_stride, int64_t PT, int max_len,
+                        int64_t head_stride, int64_t token_stride, int64_t PT, int total_blocks,
                         const uint8_t* retained, const int32_t* prank, ProblemMeta* pmeta,
                         const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
                         uint16_t* hilo, uint16_t* pkeys, int32_t* status, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   if (dtype == 0 && d == 64)
-    return run_prepare<64, false>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
-                                  prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+    return run_prepare<64, false>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
+                                  retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
+                                  status, st);
   if (dtype == 0 && d == 128)
-    return run_prepare<128, false>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
-                                   prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+    return run_prepare<128, false>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
+                                   retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
+                                   status, st);
   if (dtype == 1 && d == 64)
-    return run_prepare<64, true>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
-                                 prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+    return run_prepare<64, true>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
+                                 retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
+                                 status, st);
   if (dtype == 1 && d == 128)
-    return run_prepare<128, true>(keys, n_heads, T, head_stride, token_stride, PT, max_len, retained,
-                                  prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, st);
+    return run_prepare<128, true>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
+                                  retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
+                                  status, st);
   return hipErrorInvalidValue;
 }
 

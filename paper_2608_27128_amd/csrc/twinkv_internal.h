@@ -18,7 +18,7 @@ struct SeqInfo {
   int32_t sorted_seq;  // sequence at rank r (longest first)
   int32_t tile_cum;    // row-block tiles of ranks < r
   int32_t nb;          // row-block tiles of the sequence at rank r
-  int32_t pad;
+  int32_t prep_blk0;   // first key-preparation workgroup of sequence s (K1b grid)
 };
 
 // Per-problem result of the partition step.
@@ -60,8 +60,11 @@ int launch_partition(const uint8_t* retained, const SeqInfo* seqtab, int n_heads
 // rinv and to rcol at the key's column slot, the key copied to pkeys[h][PT][dcol] at that slot
 // (bf16; dcol = 2d bf16 hi/lo for fp32 keys, which also go to the row plane hilo
 // [n_heads][T][2d]); a non-finite key sets the problem's flag and status.
+// Tokens one K1b workgroup prepares for this (dtype, d); sequence s owns workgroups
+// [seqtab[s].prep_blk0, seqtab[s].prep_blk0 + ceil(len / that)) of each head.
+int prepare_tokens_per_block(int dtype, int d);
 int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t T,
-                        int64_t head_stride, int64_t token_stride, int64_t PT, int max_len,
+                        int64_t head_stride, int64_t token_stride, int64_t PT, int total_blocks,
                         const uint8_t* retained, const int32_t* prank, ProblemMeta* pmeta,
                         const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
                         uint16_t* hilo, uint16_t* pkeys, int32_t* status, void* stream);
