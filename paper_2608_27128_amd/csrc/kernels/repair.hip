@@ -7,10 +7,11 @@
 //
 // Since m = min(|O|, |D|), at least one side is taken whole; the other side needs the
 // m-th smallest key, found by an MSB-first radix select (11/11/10-bit digits, LDS
-// histograms) on order-preserving float keys, then a block-wide scan in position order to
-// take exactly the remaining members equal to that key.  1024 threads per problem (256 when
-// every sequence is short); every
-// pass streams b and S0 (5 bytes per token).
+// histograms) on order-preserving float keys, then a pass in position order that takes exactly
+// the remaining members equal to that key (ranked by wave ballots, slab by slab).  1024
+// threads per problem (256 when every sequence is short).  For sequences of up to 32768
+// tokens, b and S0 are read from HBM once (5 bytes per token) into LDS and every later pass
+// reads LDS; longer ones stream them from global memory on every pass.
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"
@@ -25,11 +26,17 @@ __device__ inline uint32_t ord_key(float x) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-template <int NT>
+// CAP > 0: the problem's b and S0 (as a bit array) are copied to LDS in the first pass, so
+// HBM is read once and the selection passes run from LDS (sequences of at most CAP tokens).
+// CAP = 0: every pass reads global memory.
+template <int NT, int CAP>
 __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
+  static_assert(CAP % NT == 0 && CAP % 64 == 0, "the cache holds whole slabs");
   __shared__ int s_wave[NT / 64];
   __shared__ int s_hist[kSelBins];
   __shared__ int s_pick[2];
+  __shared__ float s_b[CAP > 0 ? CAP : 1];
+  __shared__ uint32_t s_r[CAP > 0 ? CAP / 32 : 1];
 
   const int q = blockIdx.x;
   const int h = q / a.n_seqs;
@@ -43,26 +50,49 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
   const float tau = a.tau;
   const int rec0 = len - a.n_recent;  // first recent-window position
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   auto is_orphan = [&](int t, float x, bool r) { return !r && x < tau; };
   auto is_donor = [&](int t, float x, bool r) {
     return r && !(t < a.n_sink || t >= rec0) && x >= tau;
   };
+  auto bval = [&](int t) -> float {
+    if constexpr (CAP > 0) return s_b[t];
+    else return b[t];
+  };
+  auto rbit = [&](int t) -> bool {
+    if constexpr (CAP > 0) return (s_r[t >> 5] >> (t & 31)) & 1u;
+    else return s0[t] != 0;
+  };
 
-  // ---- pass 1: counts ----
+  // ---- pass 1: counts (and the LDS copy), in slabs of NT consecutive tokens ----
   int c_ret = 0, c_o = 0, c_d = 0, bad = 0;
-  for (int t = tid; t < len; t += NT) {
-    const float x = b[t];
-    const bool r = s0[t] != 0;
-    bad |= !(fabsf(x) <= 3.4e38f);
-    c_ret += r;
-    c_o += is_orphan(t, x, r);
-    c_d += is_donor(t, x, r);
+  for (int t0 = 0; t0 < len; t0 += NT) {
+    const int t = t0 + tid;
+    const bool valid = t < len;
+    const float x = valid ? b[t] : 0.0f;
+    const bool r = valid && s0[t] != 0;
+    if constexpr (CAP > 0) {
+      if (valid) s_b[t] = x;
+      const uint64_t bal = __ballot(r);
+      if (lane == 0) {
+        const int w0 = (t0 + 64 * wave) >> 5;
+        s_r[w0] = (uint32_t)bal;
+        s_r[w0 + 1] = (uint32_t)(bal >> 32);
+      }
+    }
+    if (valid) {
+      bad |= !(fabsf(x) <= 3.4e38f);
+      c_ret += r;
+      c_o += is_orphan(t, x, r);
+      c_d += is_donor(t, x, r);
+    }
   }
   int tot_ret, tot_o, tot_d, tot_bad;
   (void)sel_exclusive_scan<NT>(c_ret, s_wave, tot_ret);
   (void)sel_exclusive_scan<NT>(c_o, s_wave, tot_o);
   (void)sel_exclusive_scan<NT>(c_d, s_wave, tot_d);
-  (void)sel_exclusive_scan<NT>(bad, s_wave, tot_bad);
+  (void)sel_exclusive_scan<NT>(bad, s_wave, tot_bad);  // its barriers also publish the copy
 
   int status = 0;
   if (tot_bad || (a.pmeta && (a.pmeta[q].flags & kFlagNonfinite))) status = 2;
@@ -78,8 +108,8 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
     key_cut = block_select<NT>(
         len, m,
         [&](int t, uint32_t& key) {
-          const float x = b[t];
-          const bool r = s0[t] != 0;
+          const float x = bval(t);
+          const bool r = rbit(t);
           if (sel_o) {
             key = ord_key(x);
             return is_orphan(t, x, r);
@@ -90,43 +120,49 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
         s_hist, s_wave, s_pick, take_eq);
   }
 
-  // ---- final pass: contiguous ranges per thread so equal keys are ranked by position ----
-  const int chunk = (len + NT - 1) / NT;
-  const int t0 = min(len, tid * chunk);
-  const int t1 = min(len, t0 + chunk);
-  int eq_here = 0;
-  if (sel_o || sel_d) {
-    for (int t = t0; t < t1; ++t) {
-      const float x = b[t];
-      const bool r = s0[t] != 0;
-      if (sel_o) eq_here += (is_orphan(t, x, r) && ord_key(x) == key_cut);
-      else eq_here += (is_donor(t, x, r) && ~ord_key(x) == key_cut);
+  // ---- final pass, slab by slab: members equal to the cut key are ranked by position ----
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  int eq_before = 0;
+  for (int t0 = 0; t0 < len; t0 += NT) {
+    const int t = t0 + tid;
+    const bool valid = t < len;
+    const float x = valid ? bval(t) : 0.0f;
+    const bool r = valid && rbit(t);
+    const bool orphan = valid && is_orphan(t, x, r);
+    const bool donor = valid && is_donor(t, x, r);
+    bool eq = false;
+    if (sel_o) eq = orphan && ord_key(x) == key_cut;
+    else if (sel_d) eq = donor && ~ord_key(x) == key_cut;
+    const uint64_t bal = __ballot(eq);
+    if (lane == 0) s_wave[wave] = __popcll(bal);
+    __syncthreads();
+    int rank = eq_before + __popcll(bal & below);
+#pragma unroll
+    for (int k = 0; k < NT / 64; ++k) {
+      const int c = s_wave[k];
+      rank += k < wave ? c : 0;
+      eq_before += c;
     }
-  }
-  int dummy;
-  int eq_rank = sel_exclusive_scan<NT>(eq_here, s_wave, dummy);
-  for (int t = t0; t < t1; ++t) {
-    const float x = b[t];
-    const bool r = s0[t] != 0;
+    __syncthreads();
     uint8_t out = r ? 1 : 0;
     if (m > 0) {
-      if (is_orphan(t, x, r)) {
+      if (orphan) {
         bool admit = true;
         if (sel_o) {
           const uint32_t key = ord_key(x);
-          admit = key < key_cut || (key == key_cut && eq_rank++ < take_eq);
+          admit = key < key_cut || (key == key_cut && rank < take_eq);
         }
         if (admit) out = 1;
-      } else if (is_donor(t, x, r)) {
+      } else if (donor) {
         bool evict = true;
         if (sel_d) {
           const uint32_t key = ~ord_key(x);
-          evict = key < key_cut || (key == key_cut && eq_rank++ < take_eq);
+          evict = key < key_cut || (key == key_cut && rank < take_eq);
         }
         if (evict) out = 0;
       }
     }
-    s1[t] = out;
+    if (valid) s1[t] = out;
   }
   if (tid == 0) {
     int32_t* st = a.stats + 4 * (int64_t)q;
@@ -142,11 +178,18 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
 int launch_repair(const RepairArgs& a, void* stream) {
   const int64_t P = (int64_t)a.n_heads * a.n_seqs;
   if (P == 0) return hipSuccess;
-  // short sequences: 256 threads per problem keep more problems in flight
-  if (a.max_len > 4096)
-    hipLaunchKernelGGL(repair_kernel<1024>, dim3((unsigned)P), dim3(1024), 0, (hipStream_t)stream, a);
+  hipStream_t st = (hipStream_t)stream;
+  const dim3 grid((unsigned)P);
+  // the smallest LDS copy that holds the longest sequence; short sequences use 256 threads
+  // so that more problems are in flight
+  if (a.max_len <= 4096)
+    hipLaunchKernelGGL((repair_kernel<256, 4096>), grid, dim3(256), 0, st, a);
+  else if (a.max_len <= 16384)
+    hipLaunchKernelGGL((repair_kernel<1024, 16384>), grid, dim3(1024), 0, st, a);
+  else if (a.max_len <= 32768)
+    hipLaunchKernelGGL((repair_kernel<1024, 32768>), grid, dim3(1024), 0, st, a);
   else
-    hipLaunchKernelGGL(repair_kernel<256>, dim3((unsigned)P), dim3(256), 0, (hipStream_t)stream, a);
+    hipLaunchKernelGGL((repair_kernel<1024, 0>), grid, dim3(1024), 0, st, a);
   return hipGetLastError();
 }
 

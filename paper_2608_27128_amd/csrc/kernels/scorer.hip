@@ -5,8 +5,9 @@
 // and the `budget` highest scores are retained; equal scores go to the later position first.
 // Ranking by the key  0 for protected positions, r_i + 1 otherwise  (ascending) gives the
 // same order.  The budget-th smallest key is found by an MSB-first radix select (11/11/10-bit
-// digits, LDS histograms, 1024 or 256 threads); a block-wide scan in position order then keeps the
-// last members equal to that key.  Every pass streams the counts (4 bytes per token).
+// digits, LDS histograms, 1024 or 256 threads); a pass in position order (wave ballots, slab
+// by slab) then keeps the last members equal to that key.  Sequences of up to 32768 tokens
+// read their counts from HBM once into LDS; longer ones stream them on every pass.
 //
 // Prevalence: for each threshold tau_k, the number of tokens whose best similarity outside
 // the window exceeds tau_k, i.e. that have at least one twin (Eq. 2).
@@ -20,11 +21,15 @@ namespace {
 
 constexpr int kEvThreads = 256;  // prevalence
 
-template <int NT>
+// CAP > 0: the problem's counts are copied to LDS in the first pass (sequences of at most CAP
+// tokens), so HBM is read once; CAP = 0: every pass reads global memory.
+template <int NT, int CAP>
 __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
+  static_assert(CAP % NT == 0, "the cache holds whole slabs");
   __shared__ int s_wave[NT / 64];
   __shared__ int s_hist[kSelBins];
   __shared__ int s_pick[2];
+  __shared__ uint32_t s_c[CAP > 0 ? CAP : 1];
 
   const int q = blockIdx.x;
   const int h = q / a.n_seqs;
@@ -36,14 +41,31 @@ __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
   uint8_t* out = a.retained + base;
   const int rec0 = len - a.n_recent;
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int budget = si.budget < len ? si.budget : len;
-  auto key_of = [&](int t) -> uint32_t {
-    return (t < a.n_sink || t >= rec0) ? 0u : (uint32_t)cnt[t] + 1u;
+  const float inv_n = len > 0 ? 1.0f / (float)len : 0.0f;
+  auto count_at = [&](int t) -> uint32_t {
+    if constexpr (CAP > 0) return s_c[t];
+    else return (uint32_t)cnt[t];
   };
+  auto key_of = [&](int t) -> uint32_t {
+    return (t < a.n_sink || t >= rec0) ? 0u : count_at(t) + 1u;
+  };
+
+  // ---- pass 1: the LDS copy and the Eq. 3 scores ----
+  if (CAP > 0 || a.scores) {
+    for (int t = tid; t < len; t += NT) {
+      const int32_t c = cnt[t];
+      if constexpr (CAP > 0) s_c[t] = (uint32_t)c;
+      if (a.scores) a.scores[base + t] = -(float)c * inv_n;
+    }
+  }
+  __syncthreads();
 
   // ---- radix select of the budget-th smallest key ----
   uint32_t key_cut = 0u;
-  int take_eq = 0;
+  int take_eq = 0, total_eq = 0;
   const bool cut = budget > 0 && budget < len;
   if (cut) {
     key_cut = block_select<NT>(
@@ -53,30 +75,35 @@ __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
           return true;
         },
         s_hist, s_wave, s_pick, take_eq);
+    // the last digit's histogram still holds the number of keys equal to the cut
+    total_eq = s_hist[key_cut & 1023u];
   }
 
-  // ---- final pass: contiguous ranges per thread so equal keys are ranked by position ----
-  const int span = (len + NT - 1) / NT;
-  const int t0 = min(len, tid * span);
-  const int t1 = min(len, t0 + span);
-  int eq_here = 0;
-  if (cut)
-    for (int t = t0; t < t1; ++t) eq_here += key_of(t) == key_cut;
-  int total_eq;
-  int eq_rank = sel_exclusive_scan<NT>(eq_here, s_wave, total_eq);
-  const float inv_n = len > 0 ? 1.0f / (float)len : 0.0f;
-  for (int t = t0; t < t1; ++t) {
-    uint8_t keep;
-    if (!cut) {
-      keep = budget > 0 ? 1 : 0;
-    } else {
-      const uint32_t key = key_of(t);
-      if (key < key_cut) keep = 1;
-      else if (key == key_cut) keep = (eq_rank++ >= total_eq - take_eq) ? 1 : 0;
-      else keep = 0;
+  // ---- final pass, slab by slab: the last take_eq keys equal to the cut are kept ----
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  int eq_before = 0;
+  for (int t0 = 0; t0 < len; t0 += NT) {
+    const int t = t0 + tid;
+    const bool valid = t < len;
+    const uint32_t key = valid ? key_of(t) : 0u;
+    const bool eq = cut && valid && key == key_cut;
+    const uint64_t bal = __ballot(eq);
+    if (lane == 0) s_wave[wave] = __popcll(bal);
+    __syncthreads();
+    int rank = eq_before + __popcll(bal & below);
+#pragma unroll
+    for (int k = 0; k < NT / 64; ++k) {
+      const int c = s_wave[k];
+      rank += k < wave ? c : 0;
+      eq_before += c;
     }
-    out[t] = keep;
-    if (a.scores) a.scores[base + t] = -(float)cnt[t] * inv_n;
+    __syncthreads();
+    uint8_t keep;
+    if (!cut) keep = budget > 0 ? 1 : 0;
+    else if (key < key_cut) keep = 1;
+    else if (key == key_cut) keep = rank >= total_eq - take_eq ? 1 : 0;
+    else keep = 0;
+    if (valid) out[t] = keep;
   }
   if (tid == 0) {
     int32_t* st = a.stats + 4 * (int64_t)q;
@@ -120,10 +147,16 @@ __global__ __launch_bounds__(kEvThreads) void prevalence_kernel(PrevalenceArgs a
 int launch_evict(const EvictArgs& a, void* stream) {
   const int64_t P = (int64_t)a.n_heads * a.n_seqs;
   if (P == 0) return hipSuccess;
-  if (a.max_len > 4096)
-    hipLaunchKernelGGL(evict_kernel<1024>, dim3((unsigned)P), dim3(1024), 0, (hipStream_t)stream, a);
+  hipStream_t st = (hipStream_t)stream;
+  const dim3 grid((unsigned)P);
+  if (a.max_len <= 4096)
+    hipLaunchKernelGGL((evict_kernel<256, 4096>), grid, dim3(256), 0, st, a);
+  else if (a.max_len <= 16384)
+    hipLaunchKernelGGL((evict_kernel<1024, 16384>), grid, dim3(1024), 0, st, a);
+  else if (a.max_len <= 32768)
+    hipLaunchKernelGGL((evict_kernel<1024, 32768>), grid, dim3(1024), 0, st, a);
   else
-    hipLaunchKernelGGL(evict_kernel<256>, dim3((unsigned)P), dim3(256), 0, (hipStream_t)stream, a);
+    hipLaunchKernelGGL((evict_kernel<1024, 0>), grid, dim3(1024), 0, st, a);
   return hipGetLastError();
 }
 
