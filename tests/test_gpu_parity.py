@@ -205,6 +205,40 @@ def test_repair_from_scores_random_ties(seed):
             assert st[h, s].tolist() == [r["n_orphan"], r["n_donor"], r["m"], 0]
 
 
+@pytest.mark.parametrize("lens", [[3000, 10], [9000, 4100], [20000, 0, 17], [40000, 5]],
+                         ids=["cache4096", "cache16384", "cache32768", "uncached"])
+def test_repair_from_scores_every_cache_size(lens):
+    """The selection kernel has an LDS copy of b and S0 for sequences of up to 4096, 16384 and
+    32768 tokens and reads global memory beyond that: every variant must give the oracle's
+    S1 and counts bit for bit (quantised scores, so ties at the cut are common)."""
+    import torch
+    g = np.random.default_rng(sum(lens))
+    H = 2
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    T = int(cu[-1])
+    b = (np.round(g.uniform(-1, 1, (H, T)) * 64) / 64).astype(np.float32)
+    b[g.random((H, T)) < 0.02] = -1.0
+    tau = np.float32(0.5)
+    n_sink, n_recent = 4, 16
+    s0 = np.zeros((H, T), np.uint8)
+    budget = []
+    for s, n in enumerate(lens):
+        B = (3 * n) // 10
+        budget.append(B)
+        for h in range(H):
+            s0[h, cu[s] + g.permutation(n)[:B]] = 1
+    out = binding.repair_from_scores(torch.from_numpy(b).cuda(), mask_to_device(s0), budget,
+                                     float(tau), n_sink, n_recent, cu)
+    s1 = host(out["s1"])
+    st = host(out["stats"]).reshape(H, len(lens), 4)
+    for h in range(H):
+        for s, n in enumerate(lens):
+            a, e = cu[s], cu[s + 1]
+            r = oracle.repair(b[h, a:e].astype(np.float64), s0[h, a:e], float(tau), n_sink, n_recent)
+            assert np.array_equal(s1[h, a:e], r["s1"]), (h, s)
+            assert st[h, s].tolist() == [r["n_orphan"], r["n_donor"], r["m"], 0]
+
+
 def test_repair_budget_mismatch_and_aliasing():
     import torch
     batch = synth.make_batch(small_spec(3, [400, 500], 128, "bf16", 32, 21))
