@@ -234,19 +234,117 @@ def compact_bench(args, sp, batch, keys, ret, dev) -> int:
     return 0
 
 
+def sweep_bench(args, sp, keys, dev) -> int:
+    """The budget x threshold grid of one policy (Sec. 3.4 repair per cell): the three nested
+    retained sets' b in one twinkv_nn_scores_levels call (similarity work N * |S_3| per
+    problem), then classification / ranking / swap per (budget, tau) cell from those scores.
+    For comparison, the same grid through one retained-only repair pass per budget (work
+    N * (|S_1| + |S_2| + |S_3|)) is timed as well."""
+    import numpy as np
+    import torch
+    from paper_2608_27128_amd import binding, synth
+    fracs, taus = synth.QWEN_SWEEP_BUDGETS, synth.QWEN_SWEEP_TAUS
+    sets = [synth.make_batch(sp, budget_frac=f, threads=min(16, os.cpu_count() or 1)) for f in fracs]
+    cu = sets[0].cu_seqlens
+    level_np = np.zeros(sets[0].retained.shape, np.uint8)
+    for k in range(len(fracs), 0, -1):
+        level_np[sets[k - 1].retained != 0] = k
+    level = torch.from_numpy(level_np).to(dev)
+    rets = [torch.from_numpy(b.retained).to(dev) for b in sets]
+    budgets = [b.budget for b in sets]
+    H, T = level_np.shape
+    lens = np.diff(cu).astype(np.float64)
+    s_last = float(np.sum(lens * np.asarray(budgets[-1], dtype=np.float64)))
+    pairs = float(H) * s_last                              # N * |S_3| per problem
+    flops = 2.0 * keys.shape[2] * pairs
+    lv_out = binding.nn_scores_levels(keys, level, len(fracs), sp.w, cu)
+    ws = torch.empty((int(binding.lib().twinkv_levels_workspace_bytes(
+        0 if keys.dtype == torch.bfloat16 else 1, keys.shape[2], H, len(cu) - 1,
+        binding._i64_array(cu), len(fracs), 0)),), dtype=torch.uint8, device=dev)
+
+    def grid():
+        out = binding.nn_scores_levels(keys, level, len(fracs), sp.w, cu, workspace=ws,
+                                       outputs=lv_out)
+        cells = []
+        for k in range(len(fracs)):
+            for tau in taus:
+                cells.append(binding.repair_from_scores(out["best_lvl"][k], rets[k], budgets[k],
+                                                        tau, sp.n_sink, sp.n_recent, cu))
+        return cells
+
+    def grid_separate():
+        cells = []
+        for k in range(len(fracs)):
+            r = binding.repair(keys, rets[k], budgets[k], taus[0], sp.w, sp.n_sink, sp.n_recent,
+                               cu, want_all=False)
+            cells.append(r)
+            for tau in taus[1:]:
+                cells.append(binding.repair_from_scores(r["best_ret"], rets[k], budgets[k], tau,
+                                                        sp.n_sink, sp.n_recent, cu))
+        return cells
+
+    for _ in range(args.warmup):
+        grid()
+        grid_separate()
+    torch.cuda.synchronize()
+    hev = HipEvents()
+    e0 = [hev.create() for _ in range(args.steps)]
+    e1 = [hev.create() for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        binding.profile_sim_events(e0[k], e1[k])
+        cells = grid()
+    binding.profile_sim_events(None, None)
+    torch.cuda.synchronize()
+    ms = 1000.0 * (time.perf_counter() - t0) / args.steps
+    k2_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in zip(e0, e1)]))
+    for e in e0 + e1:
+        hev.destroy(e)
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        cells_sep = grid_separate()
+    torch.cuda.synchronize()
+    ms_sep = 1000.0 * (time.perf_counter() - t0) / args.steps
+    for a, b in zip(cells, cells_sep):     # the same retained sets either way
+        assert torch.equal(a["s1"], b["s1"]) and torch.equal(a["stats"], b["stats"])
+    log(f"[bench] sweep {args.steps} steps: {ms:.3f} ms per 9-cell grid (similarity sweeps "
+        f"{k2_ms:.3f} ms); through one repair pass per budget: {ms_sep:.3f} ms")
+    achieved = flops / (k2_ms * 1e-3) / 1e12
+    result = {
+        "metric": "budget x tau grid (3 x 3 cells) of repair passes: key pairs per second of the "
+                  "similarity work it needs (N * |S_3| per problem); ms per grid",
+        "value": pairs / (ms * 1e-3), "unit": "pairs/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if keys.dtype == torch.bfloat16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": sp.name, "problems": int(H * (len(cu) - 1)), "d": int(keys.shape[2]),
+                   "budgets": [int(b[0]) for b in budgets], "taus": list(taus), "path": "sweep",
+                   "parallelism": "none"},
+        "grid_ms_one_pass_per_budget": ms_sep,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "sim_reduce_kernel (3 launches, one per level group)",
+                     "kernel_ms": k2_ms, "flops_per_launch": flops},
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="long_aniso_32k",
-                    help="tiny | llama1b_8k | qwen4b_16k | long_aniso_32k | ragged_64x")
+    ap.add_argument("--workload", default=None,
+                    help="tiny | llama1b_8k | qwen4b_16k | long_aniso_32k | ragged_64x "
+                         "(default long_aniso_32k; qwen4b_16k for --path sweep)")
     ap.add_argument("--path", default="repair",
-                    choices=["repair", "repair_s0", "scorer", "compact"],
+                    choices=["repair", "repair_s0", "scorer", "compact", "sweep"],
                     help="repair: the full repair pass (both reductions, the headline); "
                          "repair_s0: the repair pass against retained columns only; "
                          "scorer: the standalone scorer (Eq. 2 counts, Eq. 3 eviction); "
-                         "compact: KV compaction of the keys and values at S1")
+                         "compact: KV compaction of the keys and values at S1; "
+                         "sweep: the 3 budgets x 3 thresholds grid of the 16k cache")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -280,7 +378,16 @@ def main() -> int:
         del src, dst
         log(f"[bench] calibration copy of {args.copy_calibration_mib} MiB done")
 
+    if args.workload is None:
+        args.workload = "qwen4b_16k" if args.path == "sweep" else "long_aniso_32k"
     sp = synth.spec(args.workload)
+    if args.path == "sweep":
+        keys_sp = synth.make_batch(sp, threads=min(16, os.cpu_count() or 1))
+        k = keys_sp.keys
+        kt = (torch.from_numpy(k.view(np.int16)).view(torch.bfloat16) if keys_sp.dtype == "bf16"
+              else torch.from_numpy(k)).to(dev)
+        del keys_sp, k
+        return sweep_bench(args, sp, kt, dev)
     t0 = time.perf_counter()
     batch = synth.make_batch(sp, threads=min(16, os.cpu_count() or 1))
     log(f"[bench] generated {sp.name}: keys {batch.keys.shape} {batch.dtype} in "

@@ -69,6 +69,9 @@ extern "C" {
 /* Most thresholds twinkv_prevalence takes in one call. */
 #define TWINKV_MAX_TAUS 32
 
+/* Most nested retained sets twinkv_nn_scores_levels takes in one call. */
+#define TWINKV_MAX_LEVELS 4
+
 /* Per-problem status codes (stats[q][3] / status[q]). */
 #define TWINKV_PROBLEM_OK              0
 #define TWINKV_PROBLEM_BUDGET_MISMATCH 1  /* |S0| differs from the budget; S1 = S0 */
@@ -163,6 +166,37 @@ int twinkv_twin_counts(const void* keys, int dtype, int d, int n_heads, int n_se
                        const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
                        float tau, int w, int32_t* counts, int32_t* status,
                        void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * b_i(S_k) of Sec. 3.4 Eq. 4 for nested retained sets S_1 within S_2 within ... within S_L
+ * (for example the retained sets of one policy at increasing budgets), in one call.
+ * The tokens of each level group G_k = S_k minus S_{k-1} are swept once as the retained
+ * columns, so the similarity work is N * |S_L| per problem (plus N * (N - |S_L|) when the
+ * all-keys result is asked for), instead of N * (|S_1| + ... + |S_L|) for L separate calls.
+ *
+ *   level     [n_heads][T] uint8: k in 1..n_levels = the smallest set that holds the token;
+ *             0 = in none.  Values above n_levels count as 0.
+ *   n_levels  1 <= L <= TWINKV_MAX_LEVELS.
+ *   best_lvl  [n_levels][n_heads][T] fp32: b_i(S_k) (-1 if no j of S_k lies outside the
+ *             window).  Required.
+ *   arg_lvl   [n_levels][n_heads][T] int32: the maximising position, -1 if none.  Nullable.
+ *   best_all, arg_all  as in twinkv_nn_scores.  Nullable; when both are NULL the tokens in
+ *             no set are never swept as columns.
+ *   workspace twinkv_levels_workspace_bytes(dtype, d, n_heads, n_seqs, cu_seqlens,
+ *             n_levels, want_all) bytes, want_all = (best_all or arg_all given).
+ * Other arguments as in twinkv_nn_scores.  Results equal those of separate
+ * twinkv_nn_scores calls with retained = S_k, bit for bit: every value is the same
+ * computation, and equal values go to the smaller position in both.
+ */
+int twinkv_nn_scores_levels(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                            const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                            const uint8_t* level, int n_levels, int w, float* best_all,
+                            int32_t* arg_all, float* best_lvl, int32_t* arg_lvl, int32_t* status,
+                            void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Workspace bytes of twinkv_nn_scores_levels; negative (-TWINKV_E_*) on invalid arguments. */
+int64_t twinkv_levels_workspace_bytes(int dtype, int d, int n_heads, int n_seqs,
+                                      const int64_t* cu_seqlens, int n_levels, int want_all);
 
 /*
  * The standalone TwinKV scorer of Sec. 3.2: Eq. 2 twin counts, Eq. 3 scores

@@ -23,6 +23,7 @@ TWINKV_OK = 0
 TWINKV_BF16, TWINKV_F32 = 0, 1
 OP_NN_SCORES, OP_REPAIR, OP_REPAIR_FROM_SCORES, OP_TWIN_COUNTS, OP_SCORE_EVICT, OP_COMPACT = range(6)
 MAX_TAUS = 32
+MAX_LEVELS = 4
 PROBLEM_OK, PROBLEM_BUDGET_MISMATCH, PROBLEM_NONFINITE = 0, 1, 2
 
 _lib = None
@@ -47,6 +48,9 @@ SIGNATURES = {
                                 _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_prevalence": (_I, [_VP, _I, _I, _PI64, ctypes.POINTER(ctypes.c_float), _I, _VP, _VP,
                                _I64, _VP]),
+    "twinkv_nn_scores_levels": (_I, [_VP, _I, _I, _I, _I, _PI64, _I64, _I64, _VP, _I, _I, _VP,
+                                     _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
+    "twinkv_levels_workspace_bytes": (_I64, [_I, _I, _I, _I, _PI64, _I, _I]),
     "twinkv_compact": (_I, [_VP, _VP, _I, _I, _I, _I, _PI64, _I64, _I64, _I64, _I64, _VP, _PI64,
                             _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_status_string": (ctypes.c_char_p, [_I]),
@@ -196,6 +200,51 @@ def nn_scores(keys, retained=None, w: int = 32, cu_seqlens=None, *, want_arg: bo
         ws.data_ptr(), ws.numel(), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_nn_scores", rc)
+    return {k: v for k, v in out.items() if v is not None}
+
+
+def nn_scores_levels(keys, level, n_levels: int, w: int = 32, cu_seqlens=None, *,
+                     want_all: bool = False, want_arg: bool = True, workspace=None,
+                     outputs: Optional[dict] = None) -> dict:
+    """b_i(S_k) (Sec. 3.4 Eq. 4) for nested retained sets S_1 within ... within S_L given as a
+    level array (n_heads, T) uint8 (k = the smallest set holding the token, 0 = none):
+    best_lvl / arg_lvl of shape (n_levels, n_heads, T), and best_all / arg_all when
+    ``want_all``.  ``outputs`` may pass back the dict of an earlier call."""
+    torch = _torch()
+    keys, dt = _prep_keys(keys)
+    H, T, d = keys.shape
+    dev = keys.device
+    cu = _cu(cu_seqlens, T)
+    if cu[-1] != T:
+        raise ValueError("cu_seqlens[-1] must equal T")
+    n_seqs = len(cu) - 1
+    lv = _mask(level, H, T, dev, "level")
+    if lv is None:
+        raise ValueError("level is required")
+    if outputs is None:
+        out = {
+            "best_lvl": torch.empty((n_levels, H, T), dtype=torch.float32, device=dev),
+            "arg_lvl": torch.empty((n_levels, H, T), dtype=torch.int32, device=dev) if want_arg else None,
+            "best_all": torch.empty((H, T), dtype=torch.float32, device=dev) if want_all else None,
+            "arg_all": torch.empty((H, T), dtype=torch.int32, device=dev) if (want_all and want_arg) else None,
+            "status": torch.empty((H * n_seqs,), dtype=torch.int32, device=dev),
+        }
+    else:
+        out = dict(outputs)
+    cu_c = _i64_array(cu)
+    nbytes = int(lib().twinkv_levels_workspace_bytes(dt, d, H, n_seqs, cu_c, int(n_levels),
+                                                     1 if want_all else 0))
+    if nbytes < 0:
+        raise TwinKVError("twinkv_levels_workspace_bytes", -nbytes)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
+        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    rc = lib().twinkv_nn_scores_levels(
+        keys.data_ptr(), dt, d, H, n_seqs, cu_c, keys.stride(0), keys.stride(1), lv.data_ptr(),
+        int(n_levels), int(w), _ptr(out.get("best_all")), _ptr(out.get("arg_all")),
+        out["best_lvl"].data_ptr(), _ptr(out.get("arg_lvl")), _ptr(out["status"]),
+        ws.data_ptr(), ws.numel(), _stream(dev))
+    if rc != TWINKV_OK:
+        raise TwinKVError("twinkv_nn_scores_levels", rc)
     return {k: v for k, v in out.items() if v is not None}
 
 

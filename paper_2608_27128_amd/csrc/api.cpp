@@ -161,13 +161,16 @@ int max_seq_len(const int64_t* cu, int n_seqs) {
 thread_local hipEvent_t g_sim_start = nullptr;
 thread_local hipEvent_t g_sim_stop = nullptr;
 
-// K1a + K1b + K2 (shared by nn_scores and repair).
-int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_t* cu,
-               const int64_t* budget, int64_t head_stride, int64_t token_stride,
-               const uint8_t* retained, int w, float* best_all, int32_t* arg_all,
-               float* best_ret, int32_t* arg_ret, int32_t* status, char* ws, const Layout& L,
-               bool want_all, void* stream, SeqInfo** seqtab_dev, float tau = 0.0f,
-               int32_t* counts = nullptr) {
+// K1a + K1b: the sequence table, the column partition and the prepared keys, ready for K2.
+struct Prepared {
+  SimArgs args;         // everything but the outputs, w, want_all and the count mode
+  SeqInfo* seqtab = nullptr;
+};
+
+int prepare_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_t* cu,
+                   const int64_t* budget, int64_t head_stride, int64_t token_stride,
+                   const uint8_t* retained, int32_t* status, char* ws, const Layout& L,
+                   void* stream, Prepared& P) {
   int total_tiles = 0;
   const int rpb = sim_rows_per_block(dtype, d);
   int64_t prep_blocks = 0;
@@ -178,7 +181,7 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
   if (groups * total_tiles > (int64_t)INT32_MAX) return TWINKV_E_ARG;
 
   SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
-  *seqtab_dev = dtab;
+  P.seqtab = dtab;
   if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
                      (hipStream_t)stream) != hipSuccess)
     return TWINKV_E_HIP;
@@ -199,7 +202,7 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
                           hilo, pkeys, status, stream);
   if (e) return hip_status(e);
 
-  SimArgs a;
+  SimArgs& a = P.args;
   if (dtype == TWINKV_F32) {
     a.keys = hilo;
     a.head_stride = bt.T * 2 * d;
@@ -220,21 +223,56 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
   a.n_seqs = bt.n_seqs;
   a.T = bt.T;
   a.PT = bt.PT;
+  a.total_tiles = total_tiles;
+  a.w = 0;
+  a.want_all = 0;
+  a.tau = 0.0f;
+  a.counts = nullptr;
+  a.best_all = nullptr;
+  a.arg_all = nullptr;
+  a.best_ret = nullptr;
+  a.arg_ret = nullptr;
+  return TWINKV_OK;
+}
+
+// K2 on prepared keys.
+int sim_scores(const Batch& bt, int dtype, int d, int w, bool want_all, float* best_all,
+               int32_t* arg_all, float* best_ret, int32_t* arg_ret, float tau, int32_t* counts,
+               Prepared& P, void* stream) {
+  SimArgs a = P.args;
   // |i - j| <= T - 1 inside any sequence, so any w >= T behaves like w = T.
   a.w = (int)std::min<int64_t>(w, std::max<int64_t>(bt.T, 1));
   a.want_all = want_all ? 1 : 0;
   a.tau = tau;
   a.counts = counts;
-  a.total_tiles = total_tiles;
   a.best_all = best_all;
   a.arg_all = arg_all;
   a.best_ret = best_ret;
   a.arg_ret = arg_ret;
-  if (g_sim_start && hipEventRecord(g_sim_start, (hipStream_t)stream) != hipSuccess) return TWINKV_E_HIP;
-  e = launch_sim_reduce(a, dtype, d, stream);
-  if (e) return hip_status(e);
-  if (g_sim_stop && hipEventRecord(g_sim_stop, (hipStream_t)stream) != hipSuccess) return TWINKV_E_HIP;
-  return TWINKV_OK;
+  return hip_status(launch_sim_reduce(a, dtype, d, stream));
+}
+
+int record(hipEvent_t ev, void* stream) {
+  return (ev && hipEventRecord(ev, (hipStream_t)stream) != hipSuccess) ? TWINKV_E_HIP : TWINKV_OK;
+}
+
+// K1a + K1b + K2 (shared by nn_scores, repair and the scorer).
+int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_t* cu,
+               const int64_t* budget, int64_t head_stride, int64_t token_stride,
+               const uint8_t* retained, int w, float* best_all, int32_t* arg_all,
+               float* best_ret, int32_t* arg_ret, int32_t* status, char* ws, const Layout& L,
+               bool want_all, void* stream, SeqInfo** seqtab_dev, float tau = 0.0f,
+               int32_t* counts = nullptr) {
+  Prepared P;
+  int rc = prepare_scores(keys, dtype, d, bt, cu, budget, head_stride, token_stride, retained,
+                          status, ws, L, stream, P);
+  if (rc != TWINKV_OK) return rc;
+  *seqtab_dev = P.seqtab;
+  if ((rc = record(g_sim_start, stream)) != TWINKV_OK) return rc;
+  rc = sim_scores(bt, dtype, d, w, want_all, best_all, arg_all, best_ret, arg_ret, tau, counts, P,
+                  stream);
+  if (rc != TWINKV_OK) return rc;
+  return record(g_sim_stop, stream);
 }
 
 }  // namespace
@@ -458,6 +496,91 @@ int twinkv_prevalence(const float* best_all, int n_heads, int n_seqs, const int6
   pa.n_taus = n_taus;
   for (int k = 0; k < kMaxTaus; ++k) pa.taus[k] = k < n_taus ? taus[k] : 0.0f;
   return hip_status(launch_prevalence(pa, stream));
+}
+
+// Nested sets: one sub-workspace per level group (partition and prepared keys), the group
+// mask, and the per-group maxima.
+struct LevelsLayout {
+  size_t per = 0, mask = 0, gbest = 0, garg = 0, total = 0;
+  int groups = 0;
+};
+
+LevelsLayout levels_layout(int dtype, int d, const Batch& bt, int n_levels, bool want_all) {
+  LevelsLayout LL;
+  LL.groups = n_levels + (want_all ? 1 : 0);
+  LL.per = align_up(layout_for(TWINKV_OP_NN_SCORES, dtype, d, bt).total);
+  const size_t n = (size_t)bt.n_heads * (size_t)bt.T;
+  size_t off = LL.per * (size_t)LL.groups;
+  LL.mask = off;
+  off = align_up(off + n);
+  LL.gbest = off;
+  off = align_up(off + 4 * n * (size_t)LL.groups);
+  LL.garg = off;
+  off = align_up(off + 4 * n * (size_t)LL.groups);
+  LL.total = off + kAlign;
+  return LL;
+}
+
+int64_t twinkv_levels_workspace_bytes(int dtype, int d, int n_heads, int n_seqs,
+                                      const int64_t* cu_seqlens, int n_levels, int want_all) {
+  if (dtype != TWINKV_BF16 && dtype != TWINKV_F32) return -TWINKV_E_UNSUPPORTED;
+  if (d != 64 && d != 128) return -TWINKV_E_UNSUPPORTED;
+  if (n_levels < 1 || n_levels > kMaxLevels) return -TWINKV_E_ARG;
+  Batch bt;
+  const int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return -rc;
+  return (int64_t)levels_layout(dtype, d, bt, n_levels, want_all != 0).total;
+}
+
+int twinkv_nn_scores_levels(const void* keys, int dtype, int d, int n_heads, int n_seqs,
+                            const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
+                            const uint8_t* level, int n_levels, int w, float* best_all,
+                            int32_t* arg_all, float* best_lvl, int32_t* arg_lvl, int32_t* status,
+                            void* workspace, int64_t workspace_bytes, void* stream) {
+  int rc = check_keys(keys, dtype, d, head_stride, token_stride, w);
+  if (rc != TWINKV_OK) return rc;
+  if (level == nullptr || best_lvl == nullptr) return TWINKV_E_NULL;
+  if (n_levels < 1 || n_levels > kMaxLevels) return TWINKV_E_ARG;
+  Batch bt;
+  rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  const bool want_all = best_all != nullptr || arg_all != nullptr;
+  const LevelsLayout LL = levels_layout(dtype, d, bt, n_levels, want_all);
+  if (workspace == nullptr || workspace_bytes < (int64_t)LL.total) return TWINKV_E_WORKSPACE;
+  char* base = aligned_base(workspace);
+  const Layout L = layout_for(TWINKV_OP_NN_SCORES, dtype, d, bt);
+  const int64_t n = (int64_t)n_heads * bt.T;
+  uint8_t* mask = reinterpret_cast<uint8_t*>(base + LL.mask);
+  float* gbest = reinterpret_cast<float*>(base + LL.gbest);
+  int32_t* garg = reinterpret_cast<int32_t*>(base + LL.garg);
+
+  // every group's partition and key preparation first, then the similarity sweeps back to back
+  Prepared P[kMaxLevels + 1];
+  for (int g = 0; g < LL.groups; ++g) {
+    const int sel = g < n_levels ? g + 1 : 0;  // the last group: the tokens in no set
+    if (launch_select_level(level, mask, n, sel, n_levels, stream) != 0) return TWINKV_E_HIP;
+    rc = prepare_scores(keys, dtype, d, bt, cu_seqlens, nullptr, head_stride, token_stride, mask,
+                        g == 0 ? status : nullptr, base + LL.per * (size_t)g, L, stream, P[g]);
+    if (rc != TWINKV_OK) return rc;
+  }
+  if ((rc = record(g_sim_start, stream)) != TWINKV_OK) return rc;
+  for (int g = 0; g < LL.groups; ++g) {
+    rc = sim_scores(bt, dtype, d, w, /*want_all=*/false, nullptr, nullptr, gbest + g * n,
+                    garg + g * n, 0.0f, nullptr, P[g], stream);
+    if (rc != TWINKV_OK) return rc;
+  }
+  if ((rc = record(g_sim_stop, stream)) != TWINKV_OK) return rc;
+  CombineArgs ca;
+  ca.gbest = gbest;
+  ca.garg = garg;
+  ca.n_groups = LL.groups;
+  ca.n_levels = n_levels;
+  ca.n = n;
+  ca.best_lvl = best_lvl;
+  ca.arg_lvl = arg_lvl;
+  ca.best_all = best_all;
+  ca.arg_all = arg_all;
+  return hip_status(launch_combine_levels(ca, stream));
 }
 
 int twinkv_compact(const void* keys, const void* values, int dtype, int d, int n_heads,

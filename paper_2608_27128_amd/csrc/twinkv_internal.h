@@ -143,6 +143,23 @@ struct PrevalenceArgs {
 // K4b: tokens with at least one twin per threshold (best_all > tau).
 int launch_prevalence(const PrevalenceArgs& a, void* stream);
 
+// Nested retained sets: the 0/1 mask of one level group, and the merge of per-group maxima.
+constexpr int kMaxLevels = 4;
+int launch_select_level(const uint8_t* level, uint8_t* mask, int64_t n, int sel, int n_levels,
+                        void* stream);
+struct CombineArgs {
+  const float* gbest;        // [n_groups][n]: best over each level group (-1 if none)
+  const int32_t* garg;       // [n_groups][n]: its position (-1 if none)
+  int n_groups;              // n_levels, plus one for the tokens in no set (best_all)
+  int n_levels;
+  int64_t n;                 // n_heads * T
+  float* best_lvl;           // [n_levels][n] nullable
+  int32_t* arg_lvl;          // [n_levels][n] nullable
+  float* best_all;           // [n] nullable
+  int32_t* arg_all;          // [n] nullable
+};
+int launch_combine_levels(const CombineArgs& a, void* stream);
+
 // KV compaction: positions per chunk of the retained mask, one workgroup per (head, chunk).
 #ifndef TWINKV_COMPACT_CHUNK
 #define TWINKV_COMPACT_CHUNK 2048

@@ -175,6 +175,30 @@ def test_prevalence_validation():
     assert call(wsb=0) == E_WS
 
 
+def test_levels_validation():
+    L = binding.lib()
+    cu = cu_arr([0, 100])
+    w1 = L.twinkv_levels_workspace_bytes(0, 64, 2, 1, cu, 1, 0)
+    w3 = L.twinkv_levels_workspace_bytes(0, 64, 2, 1, cu, 3, 0)
+    w3a = L.twinkv_levels_workspace_bytes(0, 64, 2, 1, cu, 3, 1)
+    assert 0 < w1 < w3 < w3a
+    assert L.twinkv_levels_workspace_bytes(0, 64, 2, 1, cu, 0, 0) == -E_ARG
+    assert L.twinkv_levels_workspace_bytes(0, 64, 2, 1, cu, 5, 0) == -E_ARG
+    assert L.twinkv_levels_workspace_bytes(0, 96, 2, 1, cu, 2, 0) == -E_UNSUP
+
+    def call(keys=FAKE, level=FAKE, nl=3, w=32, bl=FAKE, wsb=1 << 40, ts=64):
+        return L.twinkv_nn_scores_levels(keys, 0, 64, 2, 1, cu_arr([0, 100]), 6400, ts, level,
+                                          nl, w, None, None, bl, None, None, FAKE, wsb, None)
+    assert call(keys=None) == E_NULL
+    assert call(level=None) == E_NULL
+    assert call(bl=None) == E_NULL
+    assert call(nl=0) == E_ARG
+    assert call(nl=5) == E_ARG
+    assert call(w=-1) == E_ARG
+    assert call(ts=60) == E_ARG
+    assert call(wsb=64) == E_WS
+
+
 def test_compact_validation():
     L = binding.lib()
 

@@ -1,0 +1,103 @@
+"""Nested retained sets in one call (Sec. 3.4 Eq. 4 for S_1 within S_2 within S_3): the HIP
+path against separate single-set calls (bit for bit: the same per-pair computations with
+the same tie rule) and against the CPU oracle under the parity protocol."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import check_scores, host, mask_to_device, to_device
+from paper_2608_27128_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+FRACS = (0.3, 0.5, 0.7)
+
+
+def nested_batch(sp):
+    """Keys and the level array of three nested retained sets from one score draw."""
+    sets = [synth.make_batch(sp, budget_frac=f, threads=16) for f in FRACS]
+    keys = sets[0].keys
+    level = np.zeros(sets[0].retained.shape, np.uint8)
+    for k in (3, 2, 1):                        # smallest set wins
+        level[sets[k - 1].retained != 0] = k
+    return sets, keys, level
+
+
+def small(H, lens, d, dtype, seed):
+    return synth.Spec(name="levels", config_id=60 + seed, n_heads=H, lens=tuple(lens), d=d,
+                      dtype=dtype, key_recipe="offset", dup_recipe="uniform", dup_frac=0.15,
+                      dup_sigma=0.02, score_recipe="recency", policy_sinks=4, policy_recent=0,
+                      tau=0.9, w=32, n_sink=4, n_recent=0, seed=seed)
+
+
+def check_equal_to_separate(sets, keys_t, level, cu, w, want_all=True):
+    out = binding.nn_scores_levels(keys_t, mask_to_device(level), 3, w, cu, want_all=want_all)
+    assert np.all(host(out["status"]) == 0)
+    for k in range(3):
+        ref = binding.nn_scores(keys_t, mask_to_device(sets[k].retained), w, cu)
+        assert np.array_equal(host(out["best_lvl"][k]), host(ref["best_ret"])), k
+        assert np.array_equal(host(out["arg_lvl"][k]), host(ref["arg_ret"])), k
+        if want_all and k == 0:
+            assert np.array_equal(host(out["best_all"]), host(ref["best_all"]))
+            assert np.array_equal(host(out["arg_all"]), host(ref["arg_all"]))
+    return out
+
+
+@pytest.mark.parametrize("H,lens,d,dtype,w", [
+    (3, [1500, 700, 0, 33], 128, "bf16", 32),
+    (2, [2049], 64, "bf16", 16),
+    (9, [900], 128, "bf16", 32),       # 9 heads: the XCD-affine schedule
+    (2, [640], 64, "f32", 8),
+])
+def test_levels_equal_separate_calls_and_oracle(H, lens, d, dtype, w):
+    sets, keys, level = nested_batch(small(H, lens, d, dtype, H + d + w))
+    cu = sets[0].cu_seqlens
+    kt = to_device(keys, dtype)
+    out = check_equal_to_separate(sets, kt, level, cu, w)
+    out2 = binding.nn_scores_levels(kt, mask_to_device(level), 3, w, cu, want_all=False)
+    assert "best_all" not in out2
+    assert np.array_equal(host(out2["best_lvl"]), host(out["best_lvl"]))
+    # oracle, every row of the first problem of each sequence
+    for s in range(len(lens)):
+        a, e = int(cu[s]), int(cu[s + 1])
+        if e == a:
+            continue
+        for k in range(3):
+            orc = oracle.nn_scores(keys[0, a:e], dtype, sets[k].retained[0, a:e], w)
+            gpu = {"best_ret": host(out["best_lvl"][k])[0, a:e],
+                   "arg_ret": host(out["arg_lvl"][k])[0, a:e]}
+            orc_ret = {kk: v for kk, v in orc.items() if kk.endswith("_ret")}
+            check_scores(gpu, orc_ret, np.arange(e - a), keys[0, a:e], dtype,
+                         sets[k].retained[0, a:e], w)
+
+
+def test_levels_above_n_levels_count_as_none():
+    """Levels above n_levels are tokens in no set: with n_levels = 2, level 3 joins level 0."""
+    sets, keys, level = nested_batch(small(2, [800], 128, "bf16", 5))
+    cu = sets[0].cu_seqlens
+    kt = to_device(keys, "bf16")
+    out = binding.nn_scores_levels(kt, mask_to_device(level), 2, 32, cu, want_all=True)
+    for k in range(2):
+        ref = binding.nn_scores(kt, mask_to_device(sets[k].retained), 32, cu)
+        assert np.array_equal(host(out["best_lvl"][k]), host(ref["best_ret"]))
+    ref = binding.nn_scores(kt, None, 32, cu)
+    assert np.array_equal(host(out["best_all"]), host(ref["best_all"]))
+    assert np.array_equal(host(out["arg_all"]), host(ref["arg_all"]))
+
+
+def test_levels_full_qwen4b_16k():
+    """The 36x8 x 16384 x 128 cache with its three nested budgets: equal to three separate
+    calls, and sampled rows against the oracle."""
+    sp = synth.spec("qwen4b_16k")
+    sets, keys, level = nested_batch(sp)
+    cu = sets[0].cu_seqlens
+    kt = to_device(keys, "bf16")
+    out = check_equal_to_separate(sets, kt, level, cu, sp.w, want_all=False)
+    rng = np.random.default_rng(9)
+    rows = np.sort(rng.choice(16384, 64, replace=False))
+    for h in (0, 287):
+        for k in range(3):
+            orc = oracle.nn_scores(keys[h], "bf16", sets[k].retained[h], sp.w, rows=rows)
+            gpu = {"best_ret": host(out["best_lvl"][k])[h], "arg_ret": host(out["arg_lvl"][k])[h]}
+            orc_ret = {kk: v for kk, v in orc.items() if kk.endswith("_ret")}
+            check_scores(gpu, orc_ret, rows, keys[h], "bf16", sets[k].retained[h], sp.w)
