@@ -258,9 +258,9 @@ def sweep_bench(args, sp, keys, dev) -> int:
     pairs = float(H) * s_last                              # N * |S_3| per problem
     flops = 2.0 * keys.shape[2] * pairs
     lv_out = binding.nn_scores_levels(keys, level, len(fracs), sp.w, cu)
-    ws = torch.empty((int(binding.lib().twinkv_levels_workspace_bytes(
-        0 if keys.dtype == torch.bfloat16 else 1, keys.shape[2], H, len(cu) - 1,
-        binding._i64_array(cu), len(fracs), 0)),), dtype=torch.uint8, device=dev)
+    dt_code = binding.TWINKV_BF16 if keys.dtype == torch.bfloat16 else binding.TWINKV_F32
+    ws = torch.empty((binding.levels_workspace_bytes(dt_code, keys.shape[2], H, cu, len(fracs),
+                                                     False),), dtype=torch.uint8, device=dev)
 
     def grid():
         out = binding.nn_scores_levels(keys, level, len(fracs), sp.w, cu, workspace=ws,

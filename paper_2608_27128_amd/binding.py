@@ -101,6 +101,16 @@ def workspace_bytes(op: int, dtype: int, d: int, n_heads: int, cu_seqlens) -> in
     return n
 
 
+def levels_workspace_bytes(dtype: int, d: int, n_heads: int, cu_seqlens, n_levels: int,
+                           want_all: bool) -> int:
+    cu = _i64_array(cu_seqlens)
+    n = int(lib().twinkv_levels_workspace_bytes(dtype, d, n_heads, len(cu) - 1, cu,
+                                                int(n_levels), 1 if want_all else 0))
+    if n < 0:
+        raise TwinKVError("twinkv_levels_workspace_bytes", -n)
+    return n
+
+
 def _event_handle(e):
     if e is None:
         return None
@@ -232,10 +242,7 @@ def nn_scores_levels(keys, level, n_levels: int, w: int = 32, cu_seqlens=None, *
     else:
         out = dict(outputs)
     cu_c = _i64_array(cu)
-    nbytes = int(lib().twinkv_levels_workspace_bytes(dt, d, H, n_seqs, cu_c, int(n_levels),
-                                                     1 if want_all else 0))
-    if nbytes < 0:
-        raise TwinKVError("twinkv_levels_workspace_bytes", -nbytes)
+    nbytes = levels_workspace_bytes(dt, d, H, cu, n_levels, want_all)
     ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
         torch.empty((nbytes,), dtype=torch.uint8, device=dev)
     rc = lib().twinkv_nn_scores_levels(
