@@ -289,3 +289,74 @@ def test_repair_skips_evicted_columns_consistently():
     lean = binding.repair(kt, rt, batch.budget, 0.9, 32, 2, 3, batch.cu_seqlens, want_all=False)
     for k in ("s1", "stats", "best_ret", "arg_ret"):
         assert np.array_equal(host(full[k]), host(lean[k])), k
+
+
+def test_long_single_sequence_131072():
+    """Maximum-size case: one problem of 131072 tokens (d=128 bf16, 4 million columns per
+    row block sweep, the selection kernel's uncached path): sampled rows of both reductions
+    against the oracle, a bit-exact logic replay of the repair on the GPU's own b, and the
+    budget."""
+    n = 131072
+    sp = synth.Spec(name="long1", config_id=97, n_heads=1, lens=(n,), d=128, dtype="bf16",
+                    key_recipe="offset", dup_recipe="uniform", dup_frac=0.1, dup_sigma=0.02,
+                    budget_frac=0.3, policy_sinks=4, policy_recent=128, tau=0.9, w=32,
+                    n_sink=4, n_recent=128, seed=3)
+    batch = synth.make_batch(sp)
+    kt, rt = to_device(batch.keys, "bf16"), mask_to_device(batch.retained)
+    out = binding.repair(kt, rt, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent,
+                         batch.cu_seqlens)
+    s1, st = host(out["s1"])[0], host(out["stats"])[0]
+    b = host(out["best_ret"])[0]
+    assert st[3] == 0 and s1.sum() == batch.budget[0]
+    r = oracle.repair(b.astype(np.float64), batch.retained[0], sp.tau, sp.n_sink, sp.n_recent)
+    assert np.array_equal(s1, r["s1"]) and st[:3].tolist() == [r["n_orphan"], r["n_donor"], r["m"]]
+    g = np.random.default_rng(4)
+    rows = np.unique(np.concatenate([[0, 1, 383, 384, n - 385, n - 1],
+                                     g.choice(n, 40, replace=False)]))
+    orc = oracle.nn_scores(batch.keys[0], "bf16", batch.retained[0], sp.w, rows=rows)
+    gpu = {k: host(out[k])[0] for k in ("best_all", "arg_all", "best_ret", "arg_ret")}
+    print("131072 tokens:", check_scores(gpu, orc, rows, batch.keys[0], "bf16",
+                                         batch.retained[0], sp.w))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_batches_vs_oracle(seed):
+    """Seeded random shapes: heads, ragged lengths (empty ones too), d, key dtype, window,
+    tau, budgets and protected regions; every row of every problem against the oracle, and
+    the repair through check_repair."""
+    g = np.random.default_rng(1000 + seed)
+    H = int(g.integers(1, 11))
+    lens = [int(x) if g.random() > 0.15 else 0 for x in g.integers(1, 900, size=int(g.integers(1, 5)))]
+    if sum(lens) == 0:
+        lens[0] = 77
+    d = int(g.choice([64, 128]))
+    dtype = "f32" if g.random() < 0.25 else "bf16"
+    w = int(g.integers(0, 70))
+    tau = float(g.uniform(0.5, 0.99))
+    n_sink, n_recent = int(g.integers(0, 6)), int(g.integers(0, 40))
+    sp = synth.Spec(name="rand", config_id=120 + seed, n_heads=H, lens=tuple(lens), d=d,
+                    dtype=dtype, key_recipe="offset", dup_recipe="uniform",
+                    dup_frac=float(g.uniform(0.0, 0.4)), dup_sigma=0.02,
+                    budget_frac=float(g.uniform(0.1, 0.9)), policy_sinks=n_sink,
+                    policy_recent=n_recent, tau=tau, w=w, n_sink=n_sink, n_recent=n_recent,
+                    seed=seed)
+    batch = synth.make_batch(sp)
+    kt, rt = to_device(batch.keys, dtype), mask_to_device(batch.retained)
+    out = binding.repair(kt, rt, batch.budget, tau, w, n_sink, n_recent, batch.cu_seqlens)
+    s1, b = host(out["s1"]), host(out["best_ret"])
+    st = host(out["stats"]).reshape(H, len(lens), 4)
+    gpu_all = {k: host(out[k]) for k in ("best_all", "arg_all", "best_ret", "arg_ret")}
+    exact = 0
+    for h in range(H):
+        for s in range(len(lens)):
+            a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
+            if e == a:
+                assert st[h, s].tolist() == [0, 0, 0, 0]
+                continue
+            k, r = batch.keys[h, a:e], batch.retained[h, a:e]
+            orc = oracle.repair_problem(k, dtype, r, batch.budget[s], tau, w, n_sink, n_recent)
+            res = check_repair(s1[h, a:e], st[h, s], b[h, a:e], orc, r, tau, n_sink, n_recent)
+            exact += res["exact"]
+            check_scores({kk: v[h, a:e] for kk, v in gpu_all.items()}, orc, np.arange(e - a), k,
+                         dtype, r, w)
+    print("random batch", seed, H, lens, d, dtype, w, round(tau, 3), "exact repairs", exact)
