@@ -360,3 +360,39 @@ def test_random_batches_vs_oracle(seed):
             check_scores({kk: v[h, a:e] for kk, v in gpu_all.items()}, orc, np.arange(e - a), k,
                          dtype, r, w)
     print("random batch", seed, H, lens, d, dtype, w, round(tau, 3), "exact repairs", exact)
+
+
+def test_many_tiny_sequences():
+    """300 sequences of 0-60 tokens per head (many problems with at most one row block and a
+    handful of columns): every row of the repair path against the oracle, and the compaction
+    of S1 against the oracle's."""
+    g = np.random.default_rng(77)
+    lens = [int(x) for x in g.integers(0, 61, size=300)]
+    sp = synth.Spec(name="tiny_many", config_id=99, n_heads=2, lens=tuple(lens), d=64,
+                    dtype="bf16", key_recipe="offset", dup_recipe="uniform", dup_frac=0.3,
+                    dup_sigma=0.02, budget_frac=0.5, policy_sinks=2, policy_recent=3, tau=0.9,
+                    w=4, n_sink=2, n_recent=3, seed=11)
+    batch = synth.make_batch(sp)
+    kt, rt = to_device(batch.keys, "bf16"), mask_to_device(batch.retained)
+    out = binding.repair(kt, rt, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent,
+                         batch.cu_seqlens)
+    s1, b = host(out["s1"]), host(out["best_ret"])
+    st = host(out["stats"]).reshape(2, len(lens), 4)
+    gpu_all = {k: host(out[k]) for k in ("best_all", "arg_all", "best_ret", "arg_ret")}
+    for h in range(2):
+        for s, n in enumerate(lens):
+            a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
+            if n == 0:
+                continue
+            k, r = batch.keys[h, a:e], batch.retained[h, a:e]
+            orc = oracle.repair_problem(k, "bf16", r, batch.budget[s], sp.tau, sp.w, sp.n_sink,
+                                        sp.n_recent)
+            check_repair(s1[h, a:e], st[h, s], b[h, a:e], orc, r, sp.tau, sp.n_sink, sp.n_recent)
+            check_scores({kk: v[h, a:e] for kk, v in gpu_all.items()}, orc, np.arange(n), k,
+                         "bf16", r, sp.w)
+    comp = binding.compact(kt, out["s1"], batch.budget, cu_seqlens=batch.cu_seqlens)
+    o = oracle.compact(batch.keys, None, s1, batch.cu_seqlens, batch.budget)
+    np.testing.assert_array_equal(host(comp["pos"]), o["pos"])
+    np.testing.assert_array_equal(host(comp["stats"]), o["stats"])
+    import torch
+    assert np.array_equal(host(comp["keys"].view(torch.int16)).view(np.uint16), o["keys"])
