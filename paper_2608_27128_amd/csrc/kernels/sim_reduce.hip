@@ -12,8 +12,9 @@
 //    holds NSUB 32-row blocks of its row keys as MFMA B operands in registers for the whole
 //    sweep (d <= 128 makes this a short-K contraction).
 //  * Column keys stream through LDS in tiles of TN = 32 * CPT columns, double buffered, from
-//    the contiguous copy in partitioned order [S0 | evicted] (K1b, K1c), so every 32-column
-//    chunk belongs to exactly one of the two reductions and tile loads are plain streams.
+//    the contiguous copy in partitioned order [S0 | evicted] written by the key preparation,
+//    so every 32-column chunk belongs to exactly one of the two reductions and tile loads
+//    are plain streams.
 //  * v_mfma_f32_32x32x16_bf16 with A = 32 column keys, B = 32 row keys gives each lane one
 //    row i (lane % 32) and 16 columns: register v holds column 8*(v/4) + 4*(lane/32) + v%4.
 //  * Row keys are pre-scaled by an exact power of two g_i so that ||g_i k_i|| is in (0.5, 1];
@@ -25,8 +26,9 @@
 //    split k = hi + lo (bf16 each) and the three products hi.hi + lo.hi + hi.lo, laid out
 //    as a contraction over 3d.
 //  * Pairs inside the window and padding columns only occur in a few chunks per wave, found
-//    by scalar range tests; those take a masked epilogue, all others a 2.5-instruction-per-
-//    element epilogue (v_fmaak, v_and_or, half a v_max3).
+//    by scalar range tests; the sweep drops their results and a masked pass redoes them at
+//    the end.  All other chunks take a 2.5-instruction-per-element epilogue (v_fmaak,
+//    v_and_or, half a v_max3).
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
