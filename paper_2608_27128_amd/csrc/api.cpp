@@ -194,8 +194,8 @@ int prepare_scores(const void* keys, int dtype, int d, const Batch& bt, const in
   uint16_t* hilo = dtype == TWINKV_F32 ? reinterpret_cast<uint16_t*>(ws + L.hilo) : nullptr;
   uint16_t* pkeys = reinterpret_cast<uint16_t*>(ws + L.pkeys);
 
-  int e = launch_partition(retained, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT, pcol, rcol, prank,
-                           pmeta, status, stream);
+  int e = launch_partition(retained, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT,
+                           max_seq_len(cu, bt.n_seqs), pcol, rcol, prank, pmeta, status, stream);
   if (e) return hip_status(e);
   e = launch_prepare_keys(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, bt.PT,
                           (int)prep_blocks, retained, prank, pmeta, dtab, bt.n_seqs, rinv, rcol,

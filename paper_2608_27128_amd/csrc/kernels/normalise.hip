@@ -37,15 +37,14 @@ __device__ inline int block_sum(int v, int* s_red) {
   return tot;
 }
 
-constexpr int kPartThreads = 256;
-
-// One workgroup per (head, sequence) problem.
-__global__ __launch_bounds__(kPartThreads) void partition_kernel(
+// One workgroup of NT threads per (head, sequence) problem (1024 for long sequences).
+template <int NT>
+__global__ __launch_bounds__(NT) void partition_kernel(
     const uint8_t* __restrict__ retained, const SeqInfo* __restrict__ seqtab, int n_seqs,
     int64_t T, int64_t PT, int32_t* __restrict__ pcol, float* __restrict__ rcol,
     int32_t* __restrict__ prank, ProblemMeta* __restrict__ pmeta, int32_t* __restrict__ status) {
-  __shared__ int s_red[kPartThreads / 64];
-  __shared__ int s_wave[kPartThreads / 64];
+  __shared__ int s_red[NT / 64];
+  __shared__ int s_wave[NT / 64];
   const int q = blockIdx.x;
   const int h = q / n_seqs;
   const int s = q - h * n_seqs;
@@ -58,8 +57,8 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
 
   int cnt = 0;
   if (ret != nullptr)
-    for (int t = threadIdx.x; t < len; t += kPartThreads) cnt += (ret[t] != 0);
-  const int n_ret = block_sum<kPartThreads>(cnt, s_red);
+    for (int t = threadIdx.x; t < len; t += NT) cnt += (ret[t] != 0);
+  const int n_ret = block_sum<NT>(cnt, s_red);
   const int ret_pad = (n_ret + kGroupAlign - 1) / kGroupAlign * kGroupAlign;
   const int n_ev = len - n_ret;
   const int ev_pad = (n_ev + kChunk - 1) / kChunk * kChunk;
@@ -67,7 +66,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   int ret_before_round = 0;
-  for (int t0 = 0; t0 < len; t0 += kPartThreads) {
+  for (int t0 = 0; t0 < len; t0 += NT) {
     const int t = t0 + threadIdx.x;
     const bool in = t < len;
     const bool r = in && ret != nullptr && ret[t] != 0;
@@ -77,7 +76,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
     __syncthreads();
     int wbase = 0, tot = 0;
 #pragma unroll
-    for (int k = 0; k < kPartThreads / 64; ++k) {
+    for (int k = 0; k < NT / 64; ++k) {
       const int c = s_wave[k];
       wbase += (k < wv) ? c : 0;
       tot += c;
@@ -91,11 +90,11 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(
     __syncthreads();
   }
   // padding columns: no position, inverse norm 0 (their keys are never used)
-  for (int k = n_ret + (int)threadIdx.x; k < ret_pad; k += kPartThreads) {
+  for (int k = n_ret + (int)threadIdx.x; k < ret_pad; k += NT) {
     pc[k] = -1;
     rc[k] = 0.0f;
   }
-  for (int k = ret_pad + n_ev + (int)threadIdx.x; k < ret_pad + ev_pad; k += kPartThreads) {
+  for (int k = ret_pad + n_ev + (int)threadIdx.x; k < ret_pad + ev_pad; k += NT) {
     pc[k] = -1;
     rc[k] = 0.0f;
   }
@@ -243,13 +242,18 @@ hipError_t run_prepare(const void* keys, int n_heads, int64_t T, int64_t hs, int
 }  // namespace
 
 int launch_partition(const uint8_t* retained, const SeqInfo* seqtab, int n_heads, int n_seqs,
-                     int64_t T, int64_t PT, int32_t* pcol, float* rcol, int32_t* prank,
-                     ProblemMeta* pmeta, int32_t* status, void* stream) {
+                     int64_t T, int64_t PT, int max_len, int32_t* pcol, float* rcol,
+                     int32_t* prank, ProblemMeta* pmeta, int32_t* status, void* stream) {
   const int64_t P = (int64_t)n_heads * n_seqs;
   if (P == 0) return hipSuccess;
-  hipLaunchKernelGGL(partition_kernel, dim3((unsigned)P), dim3(kPartThreads), 0,
-                     (hipStream_t)stream, retained, seqtab, n_seqs, T, PT, pcol, rcol, prank,
-                     pmeta, status);
+  if (max_len > 4096)
+    hipLaunchKernelGGL(partition_kernel<1024>, dim3((unsigned)P), dim3(1024), 0,
+                       (hipStream_t)stream, retained, seqtab, n_seqs, T, PT, pcol, rcol, prank,
+                       pmeta, status);
+  else
+    hipLaunchKernelGGL(partition_kernel<256>, dim3((unsigned)P), dim3(256), 0,
+                       (hipStream_t)stream, retained, seqtab, n_seqs, T, PT, pcol, rcol, prank,
+                       pmeta, status);
   return hipGetLastError();
 }
 

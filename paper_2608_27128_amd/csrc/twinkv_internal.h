@@ -53,8 +53,8 @@ struct Layout {
 // retained mask: pcol (positions, -1 for padding), prank[t] = number of S0 positions before t
 // (t = 0..len), the per-problem meta, rcol = 0 at padding, status = 0.
 int launch_partition(const uint8_t* retained, const SeqInfo* seqtab, int n_heads, int n_seqs,
-                     int64_t T, int64_t PT, int32_t* pcol, float* rcol, int32_t* prank,
-                     ProblemMeta* pmeta, int32_t* status, void* stream);
+                     int64_t T, int64_t PT, int max_len, int32_t* pcol, float* rcol,
+                     int32_t* prank, ProblemMeta* pmeta, int32_t* status, void* stream);
 
 // K1b: one pass over the keys after K1a: inverse l2 norm of every key (fp64 accumulation) to
 // rinv and to rcol at the key's column slot, the key copied to pkeys[h][PT][dcol] at that slot
