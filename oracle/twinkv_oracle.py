@@ -16,6 +16,8 @@ for KV Cache Eviction via Pairwise Key Redundancy"):
   * Sec. 2 (Fig. 1b)     prevalence: how many tokens have at least one twin, per threshold
   * Sec. 3.1             the compacted cache: only the keys and values at the retained
                          positions survive eviction, gathered in position order
+  * Sec. 3.4             diagnostics of the repair's decisions near a boundary: distance
+                         to tau, runner-up margins and the keys at each selection cut
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library:
@@ -55,6 +57,7 @@ __all__ = [
     "nn_scores", "classify", "rank_severity", "repair", "repair_problem",
     "protected_mask", "twin_counts", "redundancy_scores", "evict_by_score",
     "score_evict_problem", "prevalence", "compact_problem", "compact",
+    "exemption_diagnostics",
 ]
 
 # Rows of the similarity matrix are evaluated in independent groups so that an
@@ -207,6 +210,24 @@ def repair(b: np.ndarray, s0: np.ndarray, tau: float, n_sink: int, n_recent: int
     return {"s1": s1.astype(np.uint8), "orphan": orphan, "donor": donor,
             "n_orphan": len(O), "n_donor": len(D), "m": m,
             "orphans_ranked": O, "donors_ranked": D}
+
+
+def exemption_diagnostics(b: np.ndarray, s0: np.ndarray, tau: float, n_sink: int,
+                          n_recent: int, second: np.ndarray | None = None) -> dict:
+    """Where the repair's discrete decisions sit close to a boundary (for accounting the
+    tokens a floating-point scorer may legitimately classify or rank differently):
+    |b_i - tau| (orphan / donor tests, Sec. 3.4), b_i - runner-up (the best-twin index),
+    and the keys on both sides of each selection cut, b(O[m-1]) and b(O[m]) for the orphans
+    and b(D[m-1]) and b(D[m]) for the donors, when that side is cut (m below its size)."""
+    b = np.asarray(b, dtype=np.float64)
+    r = repair(b, s0, tau, n_sink, n_recent)
+    O, D, m = r["orphans_ranked"], r["donors_ranked"], r["m"]
+    out = {"tau_margin": np.abs(b - tau),
+           "orphan_cut": (float(b[O[m - 1]]), float(b[O[m]])) if 0 < m < len(O) else None,
+           "donor_cut": (float(b[D[m - 1]]), float(b[D[m]])) if 0 < m < len(D) else None}
+    if second is not None:
+        out["runner_up_margin"] = b - np.asarray(second, dtype=np.float64)
+    return out
 
 
 def repair_problem(keys: np.ndarray, dtype: str, s0: np.ndarray, budget: int, tau: float,

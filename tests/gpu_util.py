@@ -95,7 +95,8 @@ def check_repair(s1_gpu, stats_gpu, b_gpu, orc: dict, s0, tau: float, n_sink: in
     adm, ev = s1g & ~s0, s0 & ~s1g
     assert adm.sum() == m_g and ev.sum() == m_g
     assert not (adm & ~O_g).any() and not (ev & ~D_g).any()
-    near_tau = np.abs(b_o - tau) < tol
+    diag = oracle.exemption_diagnostics(b_o, s0, tau, n_sink, n_recent)
+    near_tau = diag["tau_margin"] < tol
     O_o, D_o = orc["orphan"], orc["donor"]
     assert not ((O_g != O_o) & ~near_tau).any(), "orphan sets differ away from tau"
     assert not ((D_g != D_o) & ~near_tau).any(), "donor sets differ away from tau"
@@ -108,13 +109,7 @@ def check_repair(s1_gpu, stats_gpu, b_gpu, orc: dict, s0, tau: float, n_sink: in
         if ev.any() and out_d.any():
             assert b_o[ev].min() >= b_o[out_d].max() - 2 * tol, "donor severity violated"
         # with no tie-class token at all, the result must be identical
-        O_rank, D_rank = orc["orphans_ranked"], orc["donors_ranked"]
-        m_o = orc["m"]
-        cut_vals = []
-        if m_o < len(O_rank) and m_o > 0:
-            cut_vals += [b_o[O_rank[m_o - 1]], b_o[O_rank[m_o]]]
-        if m_o < len(D_rank) and m_o > 0:
-            cut_vals += [b_o[D_rank[m_o - 1]], b_o[D_rank[m_o]]]
+        cut_vals = list(diag["orphan_cut"] or ()) + list(diag["donor_cut"] or ())
         near_cut = np.zeros(n, bool)
         for c in cut_vals:
             near_cut |= np.abs(b_o - c) < tol

@@ -113,6 +113,25 @@ def pin_repair_ranked(o):
         np.testing.assert_array_equal(r["s1"], case["s1"])
 
 
+def pin_exemption_diagnostics(o):
+    """The selection-cut keys of the hand-ranked cases, and the margins' definitions."""
+    fx = _load("repair_ranked.json")
+    for case in fx["cases"]:
+        b = np.asarray(case["b"])
+        dg = o.exemption_diagnostics(b, np.asarray(fx["s0"]), fx["tau"], fx["n_sink"], fx["n_recent"],
+                                     second=b - 0.25)
+        want_o, want_d = case["orphan_cut"], case["donor_cut"]
+        assert (dg["orphan_cut"] is None) == (want_o is None), case["name"]
+        assert (dg["donor_cut"] is None) == (want_d is None), case["name"]
+        if want_o is not None:
+            np.testing.assert_allclose(dg["orphan_cut"], want_o, rtol=0, atol=0)
+        if want_d is not None:
+            np.testing.assert_allclose(dg["donor_cut"], want_d, rtol=0, atol=0)
+        np.testing.assert_allclose(dg["tau_margin"][[5, 7, 13]],
+                                   [1.85, 0.0, abs(0.84 - 0.85)], rtol=0, atol=1e-15)
+        np.testing.assert_allclose(dg["runner_up_margin"], 0.25, rtol=0, atol=1e-15)
+
+
 def pin_oscillation(o):
     fx = _load("repair_oscillation.json")
     K = _one_hot_keys(fx["one_hot_of"], fx["d"])
@@ -425,5 +444,5 @@ ALL_PINS = [
     pin_budget_checked,
     pin_twin_counts_golden, pin_twin_counts_brute_force, pin_twin_counts_vs_best,
     pin_scores_eq3, pin_evict_golden, pin_evict_invariants, pin_prevalence_golden,
-    pin_compact_golden, pin_compact_invariants,
+    pin_compact_golden, pin_compact_invariants, pin_exemption_diagnostics,
 ]

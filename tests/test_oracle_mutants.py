@@ -69,6 +69,10 @@ MUTANTS = {
     "compact_overflow_truncates": ("ok = n_keep <= capacity", "ok = True; keep = keep[:capacity]"),
     "compact_values_from_keys": ("v_out[:n_keep] = np.asarray(values)[keep]", "v_out[:n_keep] = keys[keep]"),
     "compact_pos_one_based": ("pos[:n_keep] = keep", "pos[:n_keep] = keep + 1"),
+    "cut_keys_shifted": ('"orphan_cut": (float(b[O[m - 1]]), float(b[O[m]])) if 0 < m < len(O) else None',
+                         '"orphan_cut": (float(b[O[m]]), float(b[O[m]])) if 0 < m < len(O) else None'),
+    "cut_when_side_whole": ('"donor_cut": (float(b[D[m - 1]]), float(b[D[m]])) if 0 < m < len(D) else None',
+                            '"donor_cut": (float(b[D[m - 1]]), float(b[D[min(m, len(D) - 1)]])) if 0 < m <= len(D) else None'),
     "compact_seq_offset_ignored": ("k_out[h, c0[s]:c0[s + 1]] = r[\"keys\"]",
                                    "k_out[h, :cap[s]] = r[\"keys\"]"),
 }
