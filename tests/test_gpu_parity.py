@@ -396,3 +396,31 @@ def test_many_tiny_sequences():
     np.testing.assert_array_equal(host(comp["stats"]), o["stats"])
     import torch
     assert np.array_equal(host(comp["keys"].view(torch.int16)).view(np.uint16), o["keys"])
+
+
+def test_more_heads_than_one_grid_dimension():
+    """66000 (layer, head) pairs of two short sequences: the key preparation splits its head
+    dimension over two launches (65535 heads per grid row); sampled heads on both sides of
+    the split against the oracle, and the repair's budget on every problem."""
+    H = 66000
+    sp = synth.Spec(name="many_heads", config_id=98, n_heads=H, lens=(9, 5), d=64, dtype="bf16",
+                    key_recipe="offset", dup_recipe="uniform", dup_frac=0.3, dup_sigma=0.02,
+                    budget_frac=0.5, policy_sinks=1, policy_recent=1, tau=0.9, w=1, n_sink=1,
+                    n_recent=1, seed=12)
+    batch = synth.make_batch(sp, threads=16)
+    kt, rt = to_device(batch.keys, "bf16"), mask_to_device(batch.retained)
+    out = binding.repair(kt, rt, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent,
+                         batch.cu_seqlens)
+    st = host(out["stats"]).reshape(H, 2, 4)
+    assert np.all(st[:, :, 3] == 0)
+    s1 = host(out["s1"])
+    assert np.all(s1[:, :9].sum(axis=1) == batch.budget[0])
+    assert np.all(s1[:, 9:].sum(axis=1) == batch.budget[1])
+    gpu_all = {k: host(out[k]) for k in ("best_all", "arg_all", "best_ret", "arg_ret")}
+    for h in (0, 1, 65534, 65535, 65536, H - 1):
+        for s in range(2):
+            a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
+            k, r = batch.keys[h, a:e], batch.retained[h, a:e]
+            orc = oracle.nn_scores(k, "bf16", r, sp.w)
+            check_scores({kk: v[h, a:e] for kk, v in gpu_all.items()}, orc, np.arange(e - a), k,
+                         "bf16", r, sp.w)
