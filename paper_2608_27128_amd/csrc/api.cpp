@@ -170,7 +170,7 @@ struct Prepared {
 int prepare_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_t* cu,
                    const int64_t* budget, int64_t head_stride, int64_t token_stride,
                    const uint8_t* retained, int32_t* status, char* ws, const Layout& L,
-                   void* stream, Prepared& P) {
+                   bool copy_evicted, void* stream, Prepared& P) {
   int total_tiles = 0;
   const int rpb = sim_rows_per_block(dtype, d);
   int64_t prep_blocks = 0;
@@ -199,7 +199,7 @@ int prepare_scores(const void* keys, int dtype, int d, const Batch& bt, const in
   if (e) return hip_status(e);
   e = launch_prepare_keys(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, bt.PT,
                           (int)prep_blocks, retained, prank, pmeta, dtab, bt.n_seqs, rinv, rcol,
-                          hilo, pkeys, status, stream);
+                          hilo, pkeys, status, copy_evicted ? 1 : 0, stream);
   if (e) return hip_status(e);
 
   SimArgs& a = P.args;
@@ -265,7 +265,7 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
                int32_t* counts = nullptr) {
   Prepared P;
   int rc = prepare_scores(keys, dtype, d, bt, cu, budget, head_stride, token_stride, retained,
-                          status, ws, L, stream, P);
+                          status, ws, L, want_all, stream, P);
   if (rc != TWINKV_OK) return rc;
   *seqtab_dev = P.seqtab;
   if ((rc = record(g_sim_start, stream)) != TWINKV_OK) return rc;
@@ -560,7 +560,8 @@ int twinkv_nn_scores_levels(const void* keys, int dtype, int d, int n_heads, int
     const int sel = g < n_levels ? g + 1 : 0;  // the last group: the tokens in no set
     if (launch_select_level(level, mask, n, sel, n_levels, stream) != 0) return TWINKV_E_HIP;
     rc = prepare_scores(keys, dtype, d, bt, cu_seqlens, nullptr, head_stride, token_stride, mask,
-                        g == 0 ? status : nullptr, base + LL.per * (size_t)g, L, stream, P[g]);
+                        g == 0 ? status : nullptr, base + LL.per * (size_t)g, L,
+                        /*copy_evicted=*/false, stream, P[g]);
     if (rc != TWINKV_OK) return rc;
   }
   if ((rc = record(g_sim_start, stream)) != TWINKV_OK) return rc;

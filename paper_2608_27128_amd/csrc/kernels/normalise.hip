@@ -123,7 +123,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
     const uint8_t* __restrict__ retained, const int32_t* __restrict__ prank,
     ProblemMeta* __restrict__ pmeta, const SeqInfo* __restrict__ seqtab, int n_seqs,
     float* __restrict__ rinv, float* __restrict__ rcol, uint16_t* __restrict__ hilo,
-    uint16_t* __restrict__ pkeys, int32_t* __restrict__ status, int h0) {
+    uint16_t* __restrict__ pkeys, int32_t* __restrict__ status, int h0, int copy_evicted) {
   constexpr int ESZ = F32 ? 4 : 2;
   constexpr int LPT = D * ESZ / 16;
   constexpr int TPB = 256 / LPT;
@@ -162,6 +162,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
     const int pr = prank[base + (valid ? tl : 0)];
     const int p = r ? pr : ret_cols + ((valid ? tl : 0) - pr);
     uint16_t* dst = pkeys + (base + p) * DCOL;
+    const bool copy = valid && (r || copy_evicted);  // evicted columns only for all-keys sweeps
 
     double ss = 0.0;
     if constexpr (F32) {
@@ -183,8 +184,10 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
         uint16_t* row = hilo + (h * T + tt) * (2 * D) + sub * 4;
         *reinterpret_cast<uint2*>(row) = phi;
         *reinterpret_cast<uint2*>(row + D) = plo;
-        *reinterpret_cast<uint2*>(dst + sub * 4) = phi;
-        *reinterpret_cast<uint2*>(dst + D + sub * 4) = plo;
+        if (copy) {
+          *reinterpret_cast<uint2*>(dst + sub * 4) = phi;
+          *reinterpret_cast<uint2*>(dst + D + sub * 4) = plo;
+        }
       }
     } else {
       const uint32_t wds[4] = {raw[it].x, raw[it].y, raw[it].z, raw[it].w};
@@ -194,7 +197,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
         const double x1 = (double)__uint_as_float(wds[e] & 0xFFFF0000u);
         ss += x0 * x0 + x1 * x1;
       }
-      if (valid) *reinterpret_cast<uint4*>(dst + sub * 8) = raw[it];
+      if (copy) *reinterpret_cast<uint4*>(dst + sub * 8) = raw[it];
     }
 #pragma unroll
     for (int off = LPT / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, LPT);
@@ -224,7 +227,7 @@ hipError_t run_prepare(const void* keys, int n_heads, int64_t T, int64_t hs, int
                        int64_t PT, int total_blocks, const uint8_t* retained, const int32_t* prank,
                        ProblemMeta* pmeta, const SeqInfo* seqtab, int n_seqs, float* rinv,
                        float* rcol, uint16_t* hilo, uint16_t* pkeys, int32_t* status,
-                       hipStream_t st) {
+                       int copy_evicted, hipStream_t st) {
   constexpr int ESZ = F32 ? 4 : 2;
   if (total_blocks == 0 || n_heads == 0) return hipSuccess;
   for (int h0 = 0; h0 < n_heads; h0 += 65535) {  // heads along y, in slices the grid holds
@@ -232,7 +235,7 @@ hipError_t run_prepare(const void* keys, int n_heads, int64_t T, int64_t hs, int
     hipLaunchKernelGGL((prepare_keys_kernel<D, F32>), dim3((unsigned)total_blocks, (unsigned)by),
                        dim3(256), 0, st, (const uint8_t*)keys, T, hs * ESZ, ts * ESZ, PT,
                        retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status,
-                       h0);
+                       h0, copy_evicted);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -269,24 +272,25 @@ int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t
                         int64_t head_stride, int64_t token_stride, int64_t PT, int total_blocks,
                         const uint8_t* retained, const int32_t* prank, ProblemMeta* pmeta,
                         const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
-                        uint16_t* hilo, uint16_t* pkeys, int32_t* status, void* stream) {
+                        uint16_t* hilo, uint16_t* pkeys, int32_t* status, int copy_evicted,
+                        void* stream) {
   hipStream_t st = (hipStream_t)stream;
   if (dtype == 0 && d == 64)
     return run_prepare<64, false>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
                                   retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                  status, st);
+                                  status, copy_evicted, st);
   if (dtype == 0 && d == 128)
     return run_prepare<128, false>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
                                    retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                   status, st);
+                                   status, copy_evicted, st);
   if (dtype == 1 && d == 64)
     return run_prepare<64, true>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
                                  retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                 status, st);
+                                 status, copy_evicted, st);
   if (dtype == 1 && d == 128)
     return run_prepare<128, true>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
                                   retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                  status, st);
+                                  status, copy_evicted, st);
   return hipErrorInvalidValue;
 }
 

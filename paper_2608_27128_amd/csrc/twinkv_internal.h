@@ -59,7 +59,8 @@ int launch_partition(const uint8_t* retained, const SeqInfo* seqtab, int n_heads
 // K1b: one pass over the keys after K1a: inverse l2 norm of every key (fp64 accumulation) to
 // rinv and to rcol at the key's column slot, the key copied to pkeys[h][PT][dcol] at that slot
 // (bf16; dcol = 2d bf16 hi/lo for fp32 keys, which also go to the row plane hilo
-// [n_heads][T][2d]); a non-finite key sets the problem's flag and status.
+// [n_heads][T][2d]); a non-finite key sets the problem's flag and status.  With copy_evicted
+// = 0 only the S0 columns are copied (sweeps over the retained columns alone).
 // Tokens one K1b workgroup prepares for this (dtype, d); sequence s owns workgroups
 // [seqtab[s].prep_blk0, seqtab[s].prep_blk0 + ceil(len / that)) of each head.
 int prepare_tokens_per_block(int dtype, int d);
@@ -67,7 +68,8 @@ int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t
                         int64_t head_stride, int64_t token_stride, int64_t PT, int total_blocks,
                         const uint8_t* retained, const int32_t* prank, ProblemMeta* pmeta,
                         const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
-                        uint16_t* hilo, uint16_t* pkeys, int32_t* status, void* stream);
+                        uint16_t* hilo, uint16_t* pkeys, int32_t* status, int copy_evicted,
+                        void* stream);
 
 struct SimArgs {
   const void* keys;          // bf16 keys, or the hi/lo planes for fp32 keys
