@@ -19,9 +19,13 @@
 //    row i (lane % 32) and 16 columns: register v holds column 8*(v/4) + 4*(lane/32) + v%4.
 //  * Row keys are pre-scaled by an exact power of two g_i so that ||g_i k_i|| is in (0.5, 1];
 //    x = dot * r_j + 3 then lies in [2, 4), where the fp32 bit pattern is monotone and the
-//    low 4 mantissa bits can carry the register slot: one v_max_u32 reduces value and
-//    argmax together (quantum 2^-18 of the scaled similarity, far below the 1e-3 tolerance).
-//    The chunk index of a lane's running maximum is kept beside it.
+//    low mantissa bits can carry a column code: one v_max_u32 reduces value and argmax
+//    together.  With a running update per chunk the code is the register slot (4 bits,
+//    quantum 2^-18 of the scaled similarity); with one per tile of 4 chunks it also holds
+//    the chunk's place in the tile (6 bits, quantum 2^-16), so the compare-and-select of the
+//    running maximum runs once per tile instead of once per chunk.  Either quantum is far
+//    below the 1e-3 tolerance.  The first chunk of the running maximum's chunk (or tile) is
+//    kept beside it.
 //  * Products of bf16 values are exact in fp32; accumulation is fp32.  fp32 keys use the
 //    split k = hi + lo (bf16 each) and the three products hi.hi + lo.hi + hi.lo, laid out
 //    as a contraction over 3d.
@@ -41,8 +45,9 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC>
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC, int FG>
 struct Cfg {
+  static_assert(FG == 1 || FG == CPT, "results merge per chunk or per tile");
   static constexpr int WG_PER_CU = OCC * 4 / NWAVES;  // OCC waves per SIMD
   static constexpr int KSTEPS = SPLIT ? 3 * D / 16 : D / 16;
   static constexpr int DCOL = SPLIT ? 2 * D : D;      // bf16 elements per column in LDS
@@ -135,13 +140,26 @@ constexpr int kSchedValu = 0x002;
 constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
 
-// Value + slot of the best column of one lane's 16 accumulators (unmasked chunk).
-__device__ inline uint32_t chunk_best(const f32x16& acc, const float (&rv)[16]) {
+// Low bits of a packed candidate when the chunks of a group of FG chunks are merged before
+// the running update: register slot v (4 bits) and the chunk's place kc in the group,
+// coded as LOW - (16 kc + v), so that among equal values the smaller column has the larger
+// code.  FG = 1 leaves the plain slot code 15 - v.
+template <int FG>
+struct Slots {
+  static_assert(FG == 1 || FG == 2 || FG == 4, "1, 2 or 4 chunks per group");
+  static constexpr int BITS = 4 + (FG >= 2) + (FG >= 4);
+  static constexpr uint32_t LOW = (1u << BITS) - 1u;
+};
+
+// Value + code of the best column of one lane's 16 accumulators of chunk kc of its group.
+template <int FG>
+__device__ inline uint32_t chunk_best(const f32x16& acc, const float (&rv)[16], int kc) {
+  constexpr uint32_t LOW = Slots<FG>::LOW;
   uint32_t b = 0u;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const float x = fmaf(acc[v], rv[v], 3.0f);
-    b = max(b, (__float_as_uint(x) & 0xFFFFFFF0u) | (uint32_t)(15 - v));
+    b = max(b, (__float_as_uint(x) & ~LOW) | (LOW - (uint32_t)(16 * kc + v)));
   }
   return b;
 }
@@ -159,17 +177,29 @@ __device__ inline uint32_t chunk_count(const f32x16& acc, const float (&rv)[16],
   return 16u - (uint32_t)__builtin_popcount(neg);
 }
 
-// Branch-free running update: a strictly larger value (slot bits ignored) replaces the
-// running best, so an earlier chunk keeps exact ties.
-__device__ inline void run_update(uint32_t best, int gc, uint32_t& run, int& cid) {
-  const bool upd = (best >> 4) > (run >> 4);
+// Branch-free running update: a strictly larger value (code bits ignored) replaces the
+// running best, so an earlier chunk (group) keeps exact ties.  c: its first chunk.
+template <int FG>
+__device__ inline void run_update(uint32_t best, int c, uint32_t& run, int& cid) {
+  constexpr int B = Slots<FG>::BITS;
+  const bool upd = (best >> B) > (run >> B);
   run = upd ? best : run;
-  cid = upd ? gc : cid;
+  cid = upd ? c : cid;
 }
 
-template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC, bool COUNT>
+// A running best in the per-chunk form: value, slot code 15 - v, chunk index.
+template <int FG>
+__device__ inline void to_chunk_form(uint32_t& run, int& cid) {
+  constexpr uint32_t LOW = Slots<FG>::LOW;
+  const uint32_t q = LOW - (run & LOW);
+  cid += (int)(q >> 4);
+  run = (run & ~LOW) | (15u - (q & 15u));
+}
+
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC, int FG, bool COUNT>
 __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kernel(SimArgs a) {
-  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC>;
+  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC, FG>;
+  constexpr uint32_t LOW = Slots<FG>::LOW;
   static_assert(kGroupAlign % C::TN == 0, "the evicted group must start on a tile boundary");
   __shared__ __attribute__((aligned(1024))) char smem[2 * C::STAGE + C::RETIRED];
 
@@ -292,17 +322,20 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
 
   // One running maximum per row block: S0 columns are swept first, and their results are
   // parked in LDS (``retire``) when the sweep reaches the evicted columns.
-  uint32_t run[NSUB];
+  // tb: with FG = CPT, the best of the current tile's chunks so far.
+  uint32_t run[NSUB], tb[NSUB];
   int cid[NSUB];
 #pragma unroll
   for (int s = 0; s < NSUB; ++s) {
     run[s] = 0u;
+    tb[s] = 0u;
     cid[s] = 0;
   }
   bool retired_done = false;
   auto retire = [&]() {
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
+      if constexpr (!COUNT) to_chunk_form<FG>(run[s], cid[s]);
       retired[s * 64 + lane] = make_uint2(run[s], (uint32_t)cid[s]);
       run[s] = 0u;
       cid[s] = 0;
@@ -386,12 +419,23 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   int pgc = 0;
   uint32_t pmask = 0u;  // result mask of the pending chunk (zero: dropped)
 
-  auto reduce_into = [&](const f32x16& acc, const float (&rv)[16], int gc, int s, uint32_t m) {
+  // Chunk gc (chunk kc of its tile) into row block s.  With FG = CPT the chunks of a tile
+  // are merged in tb first and the tile enters the running best at ``flush``.
+  auto reduce_into = [&](const f32x16& acc, const float (&rv)[16], int gc, int kc, int s,
+                         uint32_t m) {
     if constexpr (COUNT) {
       run[s] += chunk_count(acc, rv, thr[s]) & m;
+    } else if constexpr (FG == 1) {
+      const uint32_t best = chunk_best<1>(acc, rv, 0) & m;
+      run_update<1>(best, gc, run[s], cid[s]);
     } else {
-      const uint32_t best = chunk_best(acc, rv) & m;
-      run_update(best, gc, run[s], cid[s]);
+      tb[s] = max(tb[s], chunk_best<FG>(acc, rv, kc) & m);
+    }
+  };
+  auto flush = [&](int s, int c0) {
+    if constexpr (!COUNT && FG > 1) {
+      run_update<FG>(tb[s], c0, run[s], cid[s]);
+      tb[s] = 0u;
     }
   };
 
@@ -419,7 +463,9 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
         if (pre0)
           fc[t] = *reinterpret_cast<const bf16x8*>(st + (kc + 1) * C::CHUNK_BYTES + aoff[t]);
       }
-      reduce_into(pacc, prv, pgc, NSUB - 1, pmask);
+      // the pending chunk: the previous chunk of this tile, or the last of the previous tile
+      reduce_into(pacc, prv, pgc, kc == 0 ? CPT - 1 : kc - 1, NSUB - 1, pmask);
+      if (kc == 0) flush(NSUB - 1, c0 - CPT);
       load_rv(st, kc, rcur);
 #pragma unroll
       for (int i = 0; i < C::KSTEPS; ++i) {
@@ -437,7 +483,8 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
           if (pre)
             fc[t] = *reinterpret_cast<const bf16x8*>(st + (kc + 1) * C::CHUNK_BYTES + aoff[t]);
         }
-        reduce_into(x, rcur, gc, s - 1, m);
+        reduce_into(x, rcur, gc, kc, s - 1, m);
+        if (kc == CPT - 1) flush(s - 1, c0);
 #pragma unroll
         for (int i = 0; i < C::KSTEPS; ++i) {
           __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
@@ -472,7 +519,8 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       // reduction out of the body to share it with this rare path.
       f32x16 pa = pacc;
       asm volatile("" : "+v"(pa));
-      reduce_into(pa, prv, pgc, NSUB - 1, pmask);
+      reduce_into(pa, prv, pgc, CPT - 1, NSUB - 1, pmask);
+      flush(NSUB - 1, c0 - CPT);
       pmask = 0u;
       retire();
     }
@@ -482,8 +530,13 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       else sweep_tile(std::integral_constant<int, 1>{}, c0, keep);
     }
   }
-  reduce_into(pacc, prv, pgc, NSUB - 1, pmask);
+  reduce_into(pacc, prv, pgc, CPT - 1, NSUB - 1, pmask);
+  flush(NSUB - 1, (ntiles - 1) * CPT);
   if (!retired_done) retire();          // no evicted columns were swept
+  if constexpr (!COUNT) {
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) to_chunk_form<FG>(run[s], cid[s]);
+  }
 
   // ---- masked pass: the chunks holding window pairs or padding next to real columns, read
   // straight from the column copy, with the window / padding test per element.  Chunks are
@@ -523,7 +576,7 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const float y = fmaf(x[v], rv[v], 3.0f);
-          const uint32_t u = (__float_as_uint(y) & 0xFFFFFFF0u) | (uint32_t)(15 - v);
+          const uint32_t u = (__float_as_uint(y) & ~LOW) | (uint32_t)(15 - v);
           const uint32_t ok = (uint32_t)(jv[v] >= 0) & (uint32_t)(abs(i - jv[v]) > a.w);
           best = max(best, u & (0u - ok));
         }
@@ -585,7 +638,7 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     const int cids[2] = {(int)rr.y, cid[s]};
 #pragma unroll
     for (int grp = 0; grp < 2; ++grp) {
-      uint32_t v = runs[grp] & 0xFFFFFFF0u;
+      uint32_t v = runs[grp] & ~LOW;
       int p = cids[grp] * kChunk + slot_col(15 - (int)(runs[grp] & 15u), half);
       const uint32_t v2 = __shfl_xor(v, 32);
       const int p2 = __shfl_xor(p, 32);
@@ -616,17 +669,17 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   }
 }
 
-template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC>
+template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC, int FG>
 hipError_t run(const SimArgs& a, hipStream_t st) {
-  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC>;
+  using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC, FG>;
   const int64_t groups = a.n_heads >= 8 ? 8LL * ((a.n_heads + 7) / 8) : (int64_t)a.n_heads;
   const int64_t blocks = groups * a.total_tiles;
   if (blocks == 0) return hipSuccess;
   if (a.counts != nullptr)
-    hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC, true>),
+    hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC, FG, true>),
                        dim3((unsigned)blocks), dim3(C::NT), 0, st, a);
   else
-    hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC, false>),
+    hipLaunchKernelGGL((sim_reduce_kernel<D, SPLIT, NSUB, NWAVES, CPT, OCC, FG, false>),
                        dim3((unsigned)blocks), dim3(C::NT), 0, st, a);
   return hipGetLastError();
 }
@@ -634,18 +687,19 @@ hipError_t run(const SimArgs& a, hipStream_t st) {
 }  // namespace
 
 // Tile shapes: (d, fp32 split, NSUB 32-row blocks per wave, waves per workgroup, 32-column
-// chunks per LDS tile, waves per SIMD).  Overridable at build time for tuning sweeps.
+// chunks per LDS tile, waves per SIMD, chunks merged before each running update: 1 or the
+// chunks per tile).  Overridable at build time for tuning sweeps.
 #ifndef TWINKV_CFG_BF16_128
-#define TWINKV_CFG_BF16_128 128, false, 3, 4, 4, 2
+#define TWINKV_CFG_BF16_128 128, false, 3, 4, 4, 2, 4
 #endif
 #ifndef TWINKV_CFG_BF16_64
-#define TWINKV_CFG_BF16_64 64, false, 4, 4, 2, 2
+#define TWINKV_CFG_BF16_64 64, false, 4, 4, 2, 2, 1
 #endif
 #ifndef TWINKV_CFG_F32_64
-#define TWINKV_CFG_F32_64 64, true, 1, 4, 4, 2
+#define TWINKV_CFG_F32_64 64, true, 1, 4, 4, 2, 1
 #endif
 #ifndef TWINKV_CFG_F32_128
-#define TWINKV_CFG_F32_128 128, true, 1, 4, 2, 2
+#define TWINKV_CFG_F32_128 128, true, 1, 4, 2, 2, 1
 #endif
 
 int sim_rows_per_block(int dtype, int d) {

@@ -103,8 +103,10 @@ def test_exact_duplicates_tie_to_smallest_index():
     gpu, agg = run_and_check(batch, 32, "policy", seed=7)
     # exact copies are exact ties: indices must equal the oracle's everywhere those rows are
     # unambiguous, which run_and_check has verified; also every row with a planted copy
-    # beyond the window reaches similarity 1 up to rounding
-    assert (gpu["best_all"] > 1 - 1e-5).mean() > 0.3
+    # beyond the window reaches similarity 1 up to the packing quantum (at d=128: 2^-16 of
+    # the scaled similarity, below 2^-15 = 3.05e-5 of the similarity) and rounding
+    assert (gpu["best_all"] > 1 - 4e-5).mean() > 0.3
+    assert (gpu["best_all"] < 1 + 1e-6).all()
 
 
 def test_zero_and_scaled_keys():
