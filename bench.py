@@ -435,21 +435,23 @@ def main() -> int:
     hev = HipEvents()
     k2_start = [hev.create() for _ in range(args.steps)]
     k2_stop = [hev.create() for _ in range(args.steps)]
-    st_start = torch.cuda.Event(enable_timing=True)
-    st_stop = torch.cuda.Event(enable_timing=True)
+    # per-step events on the stream the library launches on (torch's current stream)
+    st_ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    st_start.record()
+    st_ev[0].record()
     for k in range(args.steps):
         binding.profile_sim_events(k2_start[k], k2_stop[k])
         step(out, ws)
-    st_stop.record()
+        st_ev[k + 1].record()
     binding.profile_sim_events(None, None)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     ms_per_step = 1000.0 * wall / args.steps
-    ev_ms = st_start.elapsed_time(st_stop) / args.steps
-    k2_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in zip(k2_start, k2_stop)]))
+    step_ms = [st_ev[k].elapsed_time(st_ev[k + 1]) for k in range(args.steps)]
+    ev_ms = float(np.mean(step_ms))
+    k2_each = [hev.elapsed_ms(a, b) for a, b in zip(k2_start, k2_stop)]
+    k2_ms = float(np.mean(k2_each))
     for e in k2_start + k2_stop:
         hev.destroy(e)
     stats = out["stats"].cpu().numpy()
@@ -486,10 +488,14 @@ def main() -> int:
                    "n_recent": sp.n_recent, "budget": int(batch.budget[0]), "path": args.path,
                    "parallelism": "none"},
         "repair_ms_per_cache": ms_per_step,
+        "step_ms_events": {"median": float(np.median(step_ms)), "min": float(np.min(step_ms)),
+                           "max": float(np.max(step_ms))},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": profiled_traffic(sp.name) if args.path == "repair" else None,
                      "kernel": "sim_reduce_kernel", "kernel_ms": k2_ms,
+                     "kernel_ms_median": float(np.median(k2_each)),
+                     "kernel_ms_min": float(np.min(k2_each)),
                      "flops_per_launch": flops},
     }
     if not args.no_cpu_baseline:
