@@ -94,14 +94,16 @@ int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs
  *   best_all   [n_heads][T] fp32: max over j with |i-j| > w of sim(i, j); -1 if none.  Nullable.
  *   arg_all    [n_heads][T] int32: the maximising j (position in the sequence); -1 if none.
  *              On near-equal candidates the reported j is one whose similarity is within
- *              1e-5 of the maximum; on exact equality it is the smallest such j.  Nullable.
+ *              2^-15 (3.1e-5) of the maximum for bf16 keys with d = 128 and 2^-17 (7.6e-6)
+ *              otherwise; on exact equality it is the smallest such j.  Nullable.
  *   best_ret   [n_heads][T] fp32: b_i(S0) of Eq. 4 (-1 if no retained j beyond the window).
  *              Nullable; must be NULL when retained is NULL.
  *   arg_ret    [n_heads][T] int32: the maximising retained j, -1 if none.  Nullable.
  *   status     [n_heads * n_seqs] int32 TWINKV_PROBLEM_* (only OK / NONFINITE).  Nullable.
  *
  * Similarities are computed from the stored key values with fp32 accumulation; their error
- * against exact arithmetic is below 1e-4 for bf16 and fp32 keys.
+ * against exact arithmetic is below 1e-4 for bf16 and fp32 keys (this includes the rounding
+ * down of reported values by less than the tie bound above).
  */
 int twinkv_nn_scores(const void* keys, int dtype, int d, int n_heads, int n_seqs,
                      const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
