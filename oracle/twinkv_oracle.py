@@ -18,6 +18,8 @@ for KV Cache Eviction via Pairwise Key Redundancy"):
                          positions survive eviction, gathered in position order
   * Sec. 3.4             diagnostics of the repair's decisions near a boundary: distance
                          to tau, runner-up margins and the keys at each selection cut
+  * Sec. 3.1 / 3.2       the retained set of a score-based policy: the K highest scores,
+                         with the sink and recent regions at the maximum score
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library:
@@ -38,6 +40,11 @@ Readings where the paper is silent (each is exercised by a pin test):
       among equal scores the later position is retained first (recency).
   R20 the protected regions take the maximum score, so with K >= |P| they are all kept;
       with K < |P| the same order (later position first) decides among them.
+  R22 a wrapped policy's retained set from its per-token scores (Sec. 3.1 selects |S| = K
+      positions per head and layer; Sec. 3.2 gives the protected regions the maximum
+      score): protected positions first, then higher scores; equal scores and the
+      protected positions among themselves go to the lower position first; a NaN score
+      ranks below every number, and -0 equals +0.
   R21 compaction writes the kept rows of each problem in ascending position order into
       `capacity` reserved rows; rows past the kept count are zero with position -1, and
       a problem that keeps more positions than it has rows is an error (status 1) whose
@@ -57,7 +64,7 @@ __all__ = [
     "nn_scores", "classify", "rank_severity", "repair", "repair_problem",
     "protected_mask", "twin_counts", "redundancy_scores", "evict_by_score",
     "score_evict_problem", "prevalence", "compact_problem", "compact",
-    "exemption_diagnostics",
+    "exemption_diagnostics", "select_topk",
 ]
 
 # Rows of the similarity matrix are evaluated in independent groups so that an
@@ -293,6 +300,28 @@ def evict_by_score(counts: np.ndarray, budget: int, n_sink: int, n_recent: int) 
     score = np.where(protected_mask(n, n_sink, n_recent), np.inf, redundancy_scores(counts, n))
     pos = np.arange(n)
     order = np.lexsort((-pos, -score))     # score descending, then position descending
+    keep = np.zeros(n, dtype=np.uint8)
+    keep[order[:min(budget, n)]] = 1
+    return keep
+
+
+def select_topk(scores: np.ndarray, budget: int, n_sink: int, n_recent: int) -> np.ndarray:
+    """The retained set of a score-based policy (Sec. 3.1: |S| = K positions kept per head
+    and layer; Sec. 3.2: the sink and recent regions take the maximum score): the `budget`
+    best positions in the order of reading R22.  Returns a uint8 mask."""
+    sc = np.asarray(scores, dtype=np.float64)
+    n = len(sc)
+    if budget < 0:
+        raise ValueError("budget must be >= 0")
+    prot = protected_mask(n, n_sink, n_recent)
+    # the protected positions all take the maximum score (so they tie among themselves);
+    # comparisons treat -0 and +0 as equal
+    nan = np.isnan(sc) & ~prot
+    s = np.where(prot, np.inf, np.where(nan, 0.0, sc))
+    pos = np.arange(n)
+    # ascending sort keys, last one primary: protected first, non-NaN before NaN,
+    # higher score first, lower position first
+    order = np.lexsort((pos, -s, nan, ~prot))
     keep = np.zeros(n, dtype=np.uint8)
     keep[order[:min(budget, n)]] = 1
     return keep

@@ -394,6 +394,83 @@ def pin_prevalence_golden(o):
 
 
 # ----------------------------------------------------------------------------
+# Sec. 3.1 / 3.2: a score-based policy's retained set (reading R22)
+# ----------------------------------------------------------------------------
+def pin_select_golden(o):
+    fx = _load("select_topk.json")
+    scores = np.array([float(x) for x in fx["scores"]])
+    for case in fx["cases"]:
+        got = o.select_topk(scores, case["budget"], fx["n_sink"], fx["n_recent"])
+        np.testing.assert_array_equal(got, case["retained"])
+
+
+def _ahead(i, j, sc, prot):
+    """True when position j precedes position i in the retention order, decided pairwise:
+    protected before unprotected; inside the protected regions, by position; otherwise a
+    number before NaN, then the higher score, then the lower position."""
+    if prot[j] != prot[i]:
+        return bool(prot[j])
+    if prot[j]:
+        return j < i
+    nj, ni = np.isnan(sc[j]), np.isnan(sc[i])
+    if nj != ni:
+        return bool(ni)
+    if not nj and sc[j] != sc[i]:
+        return bool(sc[j] > sc[i])
+    return j < i
+
+
+def pin_select_brute_force(o):
+    """Position i is kept exactly when fewer than `budget` positions precede it (pairwise
+    comparison, no sorting), on tiny problems with many ties, signed zeros, infinities and
+    NaN; the protected regions overlap or cover everything in some draws."""
+    rng = np.random.default_rng(23)
+    pool = np.array([0.0, -0.0, 0.5, -0.5, 1.0, np.inf, -np.inf, np.nan])
+    for trial in range(300):
+        n = int(rng.integers(0, 14))
+        sc = pool[rng.integers(0, len(pool), n)]
+        n_sink, n_recent = int(rng.integers(0, 4)), int(rng.integers(0, 4))
+        budget = int(rng.integers(0, n + 3))
+        idx = np.arange(n)
+        prot = (idx < n_sink) | (idx >= n - n_recent)
+        want = np.array([sum(_ahead(i, j, sc, prot) for j in range(n) if j != i) < budget
+                         for i in range(n)], dtype=np.uint8)
+        np.testing.assert_array_equal(o.select_topk(sc, budget, n_sink, n_recent), want)
+
+
+def pin_select_invariants(o):
+    """|S| = min(K, n); the protected regions are kept when K >= |P| and only they (lowest
+    positions first) otherwise; every kept score is at least every dropped one; NaN only
+    after every number; at the cut the kept positions are the lower ones."""
+    rng = np.random.default_rng(29)
+    for trial in range(200):
+        n = int(rng.integers(1, 60))
+        sc = np.round(rng.standard_normal(n), 1)          # many exact ties
+        sc[rng.random(n) < 0.1] = np.nan
+        n_sink, n_recent = int(rng.integers(0, 5)), int(rng.integers(0, 5))
+        budget = int(rng.integers(0, n + 3))
+        keep = o.select_topk(sc, budget, n_sink, n_recent).astype(bool)
+        assert keep.sum() == min(budget, n)
+        idx = np.arange(n)
+        prot = (idx < n_sink) | (idx >= n - n_recent)
+        if budget >= prot.sum():
+            assert keep[prot].all()
+        else:
+            assert np.array_equal(idx[keep], idx[prot][:budget])
+            continue
+        free = ~prot
+        kept, ev = keep & free, ~keep & free
+        if (kept & np.isnan(sc)).any():
+            assert not (ev & ~np.isnan(sc)).any()
+        kn, en = kept & ~np.isnan(sc), ev & ~np.isnan(sc)
+        if kn.any() and en.any():
+            assert sc[kn].min() >= sc[en].max()
+            cut = sc[kn].min()
+            if (en & (sc == cut)).any():
+                assert idx[kn & (sc == cut)].max() < idx[en & (sc == cut)].min()
+
+
+# ----------------------------------------------------------------------------
 # Sec. 3.1: the compacted cache
 # ----------------------------------------------------------------------------
 def pin_compact_golden(o):
@@ -445,4 +522,5 @@ ALL_PINS = [
     pin_twin_counts_golden, pin_twin_counts_brute_force, pin_twin_counts_vs_best,
     pin_scores_eq3, pin_evict_golden, pin_evict_invariants, pin_prevalence_golden,
     pin_compact_golden, pin_compact_invariants, pin_exemption_diagnostics,
+    pin_select_golden, pin_select_brute_force, pin_select_invariants,
 ]

@@ -61,6 +61,17 @@ MUTANTS = {
                           "score = redundancy_scores(counts, n)"),
     "evict_budget_off_by_one": ("keep[order[:min(budget, n)]] = 1", "keep[order[:min(budget + 1, n)]] = 1"),
     "prevalence_ge": ("np.sum(b > float(t))", "np.sum(b >= float(t))"),
+    # Sec. 3.1 / 3.2 policy selection (reading R22)
+    "select_tie_later": ("order = np.lexsort((pos, -s, nan, ~prot))",
+                         "order = np.lexsort((-pos, -s, nan, ~prot))"),
+    "select_ascending": ("order = np.lexsort((pos, -s, nan, ~prot))",
+                         "order = np.lexsort((pos, s, nan, ~prot))"),
+    "select_nan_first": ("order = np.lexsort((pos, -s, nan, ~prot))",
+                         "order = np.lexsort((pos, -s, ~nan, ~prot))"),
+    "select_unprotected": ("order = np.lexsort((pos, -s, nan, ~prot))",
+                           "order = np.lexsort((pos, -s, nan))"),
+    "select_protected_by_score": ("s = np.where(prot, np.inf, np.where(nan, 0.0, sc))",
+                                  "s = np.where(nan, 0.0, sc)"),
     # Sec. 3.1 compaction
     "compact_reversed": ("keep = np.flatnonzero(np.asarray(retained) != 0)",
                          "keep = np.flatnonzero(np.asarray(retained) != 0)[::-1]"),
