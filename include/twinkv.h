@@ -224,6 +224,28 @@ int twinkv_score_evict(const void* keys, int dtype, int d, int n_heads, int n_se
                        void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
+ * A score-based policy's retained set (Sec. 3.1: a policy keeps |S| = K positions per head
+ * and layer; Sec. 3.2: the sink and recent regions take the maximum score): per problem,
+ * the budget positions first in this order: protected positions (by position), then higher
+ * scores, equal scores by lower position, NaN scores after every number (-0 equals +0).
+ * With budget >= len every token is kept; with budget 0 none.  The result is the S0 that
+ * twinkv_repair takes, so a wrapped policy that computes per-token scores on the GPU
+ * (attention mass, an expected-attention estimate, a recency score) stays on the GPU.
+ *
+ *   scores        [n_heads][T] fp32 (any values, NaN and infinities included).
+ *   budget        (host) [n_seqs] int64 >= 0: tokens to keep per problem of sequence s.
+ *   retained_out  [n_heads][T] uint8, receives the kept set as 0/1 (required).
+ *   stats         [n_heads * n_seqs][4] int32 = {tokens kept, NaN scores, 0, 0}.  Nullable.
+ *   workspace     twinkv_workspace_bytes(TWINKV_OP_REPAIR_FROM_SCORES, ...) bytes (the
+ *                 sequence table).
+ * Errors: NULL scores / budget / retained_out, a negative n_sink / n_recent or budget, or a
+ * malformed cu_seqlens are rejected before anything is enqueued.
+ */
+int twinkv_select_topk(const float* scores, int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                       const int64_t* budget, int n_sink, int n_recent, uint8_t* retained_out,
+                       int32_t* stats, void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
  * Twin prevalence (Sec. 2, Fig. 1b): for every problem q and threshold taus[k],
  *   out[q][k] = #{ tokens i of q : best_all[i] > taus[k] },
  * the number of tokens with at least one twin at that threshold (Eq. 2), from best_all as

@@ -48,6 +48,7 @@ SIGNATURES = {
                                 _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_prevalence": (_I, [_VP, _I, _I, _PI64, ctypes.POINTER(ctypes.c_float), _I, _VP, _VP,
                                _I64, _VP]),
+    "twinkv_select_topk": (_I, [_VP, _I, _I, _PI64, _PI64, _I, _I, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_nn_scores_levels": (_I, [_VP, _I, _I, _I, _I, _PI64, _I64, _I64, _VP, _I, _I, _VP,
                                      _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_levels_workspace_bytes": (_I64, [_I, _I, _I, _I, _PI64, _I, _I]),
@@ -391,6 +392,41 @@ def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_score_evict", rc)
     return {k: v for k, v in out.items() if v is not None}
+
+
+def select_topk(scores, budget, n_sink: int = 4, n_recent: int = 64, cu_seqlens=None, *,
+                workspace=None, outputs: Optional[dict] = None) -> dict:
+    """A score-based policy's retained set (Sec. 3.1 / 3.2): per problem the ``budget[s]``
+    positions first in the order protected, higher score, lower position (NaN last).
+    scores: float32 (n_heads, T) on the GPU.  Returns retained uint8 (n_heads, T) and
+    stats int32 (n_heads * n_seqs, 4) = {kept, NaN scores, 0, 0}."""
+    torch = _torch()
+    if scores.dim() == 1:
+        scores = scores.unsqueeze(0)
+    if scores.dtype != torch.float32 or not scores.is_cuda:
+        raise ValueError("scores must be a float32 GPU tensor")
+    scores = scores.contiguous()
+    H, T = scores.shape
+    dev = scores.device
+    cu = _cu(cu_seqlens, T)
+    if cu[-1] != T:
+        raise ValueError("cu_seqlens[-1] must equal T")
+    n_seqs = len(cu) - 1
+    bud = np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,))
+    out = outputs if outputs is not None else {
+        "retained": torch.empty((H, T), dtype=torch.uint8, device=dev),
+        "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
+    }
+    nbytes = workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
+        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    rc = lib().twinkv_select_topk(
+        scores.data_ptr(), H, n_seqs, _i64_array(cu), _i64_array(bud), int(n_sink),
+        int(n_recent), out["retained"].data_ptr(), _ptr(out["stats"]), ws.data_ptr(),
+        ws.numel(), _stream(dev))
+    if rc != TWINKV_OK:
+        raise TwinKVError("twinkv_select_topk", rc)
+    return out
 
 
 def prevalence(best_all, taus, cu_seqlens=None) -> "torch.Tensor":

@@ -1,7 +1,7 @@
 // Host layer of the C ABI declared in include/twinkv.h: argument validation (pure host code,
 // done before anything is enqueued), workspace layout, the per-sequence schedule table and
 // the kernel launches (K1a partition, K1b key preparation, K2 similarity, K3 repair, K4 scorer
-// eviction and prevalence, K5 KV compaction).
+// eviction, policy selection and prevalence, K5 KV compaction).
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -455,11 +455,49 @@ int twinkv_score_evict(const void* keys, int dtype, int d, int n_heads, int n_se
   if (rc != TWINKV_OK) return rc;
   EvictArgs ea;
   ea.counts = c;
+  ea.in_scores = nullptr;
   ea.retained = retained_out;
   ea.scores = scores;
   ea.stats = stats;
   ea.seqtab = dtab;
   ea.pmeta = reinterpret_cast<const ProblemMeta*>(ws + L.pmeta);
+  ea.n_heads = n_heads;
+  ea.n_seqs = n_seqs;
+  ea.T = bt.T;
+  ea.n_sink = n_sink;
+  ea.n_recent = n_recent;
+  ea.max_len = max_seq_len(cu_seqlens, n_seqs);
+  return hip_status(launch_evict(ea, stream));
+}
+
+int twinkv_select_topk(const float* scores, int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                       const int64_t* budget, int n_sink, int n_recent, uint8_t* retained_out,
+                       int32_t* stats, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (scores == nullptr || budget == nullptr || retained_out == nullptr) return TWINKV_E_NULL;
+  if (n_sink < 0 || n_recent < 0) return TWINKV_E_ARG;
+  Batch bt;
+  int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  for (int s = 0; s < n_seqs; ++s) {
+    if (budget[s] < 0 || budget[s] > INT32_MAX) return TWINKV_E_ARG;
+  }
+  const Layout L = layout_for(TWINKV_OP_REPAIR_FROM_SCORES, 0, 64, bt);
+  if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
+  char* ws = aligned_base(workspace);
+  int tiles = 0;
+  std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, budget, 0, tiles);
+  SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
+  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
+                     (hipStream_t)stream) != hipSuccess)
+    return TWINKV_E_HIP;
+  EvictArgs ea;
+  ea.counts = nullptr;
+  ea.in_scores = scores;
+  ea.retained = retained_out;
+  ea.scores = nullptr;
+  ea.stats = stats;
+  ea.seqtab = dtab;
+  ea.pmeta = nullptr;
   ea.n_heads = n_heads;
   ea.n_seqs = n_seqs;
   ea.T = bt.T;

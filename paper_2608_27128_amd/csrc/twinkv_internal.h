@@ -118,7 +118,8 @@ struct RepairArgs {
 int launch_repair(const RepairArgs& a, void* stream);
 
 struct EvictArgs {
-  const int32_t* counts;     // [n_heads][T] Eq. 2 twin counts
+  const int32_t* counts;     // [n_heads][T] Eq. 2 twin counts (scorer)
+  const float* in_scores;    // [n_heads][T] a policy's scores (policy selection), else null
   uint8_t* retained;         // [n_heads][T] out: kept set
   float* scores;             // nullable [n_heads][T] out: Eq. 3 scores
   int32_t* stats;            // [n_heads * n_seqs][4]
@@ -129,7 +130,8 @@ struct EvictArgs {
   int n_sink, n_recent;
   int max_len;               // longest sequence (picks the workgroup size)
 };
-// K4a: the standalone scorer's retained set (the budget highest Eq. 3 scores).
+// K4a: the standalone scorer's retained set (the budget highest Eq. 3 scores), or with
+// in_scores a score-based policy's retained set.
 int launch_evict(const EvictArgs& a, void* stream);
 
 constexpr int kMaxTaus = 32;

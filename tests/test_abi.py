@@ -175,6 +175,24 @@ def test_prevalence_validation():
     assert call(wsb=0) == E_WS
 
 
+def test_select_topk_validation():
+    L = binding.lib()
+
+    def call(scores=FAKE, budget=(10, 20), ns=4, nr=8, out=FAKE, cu=(0, 100, 150), wsb=1 << 30):
+        return L.twinkv_select_topk(scores, 2, len(cu) - 1, cu_arr(list(cu)),
+                                    None if budget is None else cu_arr(list(budget)), ns, nr, out,
+                                    None, FAKE, wsb, None)
+    assert call(scores=None) == E_NULL
+    assert call(out=None) == E_NULL
+    assert call(budget=None) == E_NULL
+    assert call(ns=-1) == E_ARG
+    assert call(nr=-2) == E_ARG
+    assert call(budget=(10, -1)) == E_ARG
+    assert call(cu=(0, 100, 90)) == E_ARG           # decreasing offsets
+    assert call(cu=(5, 100, 150)) == E_ARG          # first offset not 0
+    assert call(wsb=0) == E_WS
+
+
 def test_levels_validation():
     L = binding.lib()
     cu = cu_arr([0, 100])
