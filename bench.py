@@ -234,6 +234,102 @@ def compact_bench(args, sp, batch, keys, ret, dev) -> int:
     return 0
 
 
+def pipeline_bench(args, sp, batch, keys, dev) -> int:
+    """The eviction pipeline end to end on the GPU: a wrapped policy's per-token scores ->
+    S0 (twinkv_select_topk, Sec. 3.1 / 3.2) -> the repair pass against the retained columns
+    (Sec. 3.4, only b is needed) -> S1 -> the compacted keys and values (Sec. 3.1).  Scores
+    are seeded U(0,1) draws on the device, the synthetic policy's distribution.  Value
+    vectors as in the compaction bench.  The timed step is the three calls."""
+    import numpy as np
+    import torch
+    from paper_2608_27128_amd import binding
+    cu = batch.cu_seqlens
+    H, T = batch.retained.shape
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    scores = torch.rand((H, T), generator=gen, device=dev, dtype=torch.float32)
+    ibits = torch.int16 if keys.dtype == torch.bfloat16 else torch.int32
+    pattern = 0x5A5A if ibits == torch.int16 else 0x5A5A5A5A
+    vals = (keys.view(ibits) ^ pattern).view(keys.dtype)
+    cap = np.asarray(batch.budget, dtype=np.int64)
+    dt_code = 0 if batch.dtype == "bf16" else 1
+    ws = torch.empty((max(binding.workspace_bytes(binding.OP_REPAIR, dt_code, batch.d, H, cu),
+                          binding.workspace_bytes(binding.OP_COMPACT, 0, batch.d, H, cu)),),
+                     dtype=torch.uint8, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4 * args.steps)]
+
+    def step(outs=None, k=None):
+        o = outs or {}
+        if k is not None:
+            ev[4 * k].record()
+        o["sel"] = binding.select_topk(scores, cap, sp.n_sink, sp.n_recent, cu, workspace=ws,
+                                       outputs=o.get("sel"))
+        if k is not None:
+            ev[4 * k + 1].record()
+        o["rep"] = binding.repair(keys, o["sel"]["retained"], cap, sp.tau, sp.w, sp.n_sink,
+                                  sp.n_recent, cu, want_all=False, outputs=o.get("rep"),
+                                  workspace=ws)
+        if k is not None:
+            ev[4 * k + 2].record()
+        o["comp"] = binding.compact(keys, o["rep"]["s1"], cap, values=vals, cu_seqlens=cu,
+                                    outputs=o.get("comp"), workspace=ws)
+        if k is not None:
+            ev[4 * k + 3].record()
+        return o
+    out = step()
+    for _ in range(args.warmup):
+        step(out)
+    torch.cuda.synchronize()
+    hev = HipEvents()
+    k0 = [hev.create() for _ in range(args.steps)]
+    k1 = [hev.create() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        binding.profile_sim_events(k0[k], k1[k])     # K2 of the repair (compact: its gather)
+        step(out, k)
+    binding.profile_sim_events(None, None)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_per_step = 1000.0 * wall / args.steps
+    stage = np.array([[ev[4 * k + i].elapsed_time(ev[4 * k + i + 1]) for i in range(3)]
+                      for k in range(args.steps)])
+    k_ms = [hev.elapsed_ms(a, b) for a, b in zip(k0, k1)]
+    for e in k0 + k1:
+        hev.destroy(e)
+    assert (out["sel"]["stats"][:, 0].cpu().numpy() == np.repeat(cap[None, :], H, 0).ravel()).all()
+    assert (out["rep"]["stats"][:, 3].cpu().numpy() == 0).all()
+    assert (out["comp"]["stats"][:, 2].cpu().numpy() == 0).all()
+    sel_ms, rep_ms, comp_ms = (float(x) for x in np.median(stage, axis=0))
+    lens = np.diff(cu).astype(np.float64)
+    flops = 2.0 * batch.d * sp.n_heads * float(np.sum(lens * cap))     # retained columns only
+    # the last profiled span of a step is the compaction's gather; K2 is timed by its stage
+    achieved = flops / (rep_ms * 1e-3) / 1e12
+    log(f"[bench] pipeline {args.steps} steps: {ms_per_step:.3f} ms/step; select {sel_ms:.3f} ms, "
+        f"repair {rep_ms:.3f} ms, compact {comp_ms:.3f} ms (medians of per-stage events)")
+    result = {
+        "metric": "eviction pipeline (policy scores -> S0 -> repair -> S1 -> compacted K/V): "
+                  "cache tokens per second",
+        "value": float(H * T) / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if batch.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": sp.name, "problems": int(sp.n_heads * sp.n_seqs),
+                   "d": int(batch.d), "budget": int(cap[0]), "path": "pipeline",
+                   "parallelism": "none"},
+        "stage_ms": {"select_topk": sel_ms, "repair_retained_columns": rep_ms,
+                     "compact": comp_ms},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "repair pass (K1a + K1b + K2 on the retained columns + K3)",
+                     "kernel_ms": rep_ms, "flops_per_launch": flops,
+                     "gather_ms": float(np.median(k_ms))},
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def sweep_bench(args, sp, keys, dev) -> int:
     """The budget x threshold grid of one policy (Sec. 3.4 repair per cell): the three nested
     retained sets' b in one twinkv_nn_scores_levels call (similarity work N * |S_3| per
@@ -339,12 +435,13 @@ def main() -> int:
                     help="tiny | llama1b_8k | qwen4b_16k | long_aniso_32k | ragged_64x "
                          "(default long_aniso_32k; qwen4b_16k for --path sweep)")
     ap.add_argument("--path", default="repair",
-                    choices=["repair", "repair_s0", "scorer", "compact", "sweep"],
+                    choices=["repair", "repair_s0", "scorer", "compact", "sweep", "pipeline"],
                     help="repair: the full repair pass (both reductions, the headline); "
                          "repair_s0: the repair pass against retained columns only; "
                          "scorer: the standalone scorer (Eq. 2 counts, Eq. 3 eviction); "
                          "compact: KV compaction of the keys and values at S1; "
-                         "sweep: the 3 budgets x 3 thresholds grid of the 16k cache")
+                         "sweep: the 3 budgets x 3 thresholds grid of the 16k cache; "
+                         "pipeline: policy scores -> S0 -> repair -> S1 -> compacted K/V")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -411,6 +508,8 @@ def main() -> int:
 
     if args.path == "compact":
         return compact_bench(args, sp, batch, keys, ret, dev)
+    if args.path == "pipeline":
+        return pipeline_bench(args, sp, batch, keys, dev)
 
     if args.path in ("repair", "repair_s0"):
         want_all = args.path == "repair"
