@@ -13,6 +13,9 @@
  *   - the standalone scorer (Sec. 3.2, Eq. 2-3): twin counts r_i, scores s_i = -r_i / n, and
  *     the retained set of the K highest scores with the sink / recent regions kept first;
  *   - the prevalence statistic of Sec. 2 (Fig. 1b): tokens with at least one twin;
+ *   - a wrapped policy's retained set from its per-token scores (Sec. 3.1: K positions per
+ *     head and layer; Sec. 3.2: the sink / recent regions at the maximum score), the S0 the
+ *     repair takes;
  *   - KV compaction (Sec. 3.1): only the keys and values at the retained positions are kept
  *     for generation, gathered here into a dense cache.
  *
