@@ -286,6 +286,12 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   // and chunks past the last one.  Branch-free scalar arithmetic, so the tile body stays
   // one straight-line block.
   auto keep_bits = [&](int c0) -> uint32_t {
+    // most tiles drop nothing: one range test over the whole tile
+    const int c1 = c0 + CPT - 1;
+    const bool clean = (c1 < nchunks) && !(c1 >= ret_real && c0 < ret_chunks) &&
+                       !(c1 >= cr_lo && c0 <= cr_hi) && !(c1 >= ce_lo && c0 <= ce_hi) &&
+                       !(pad_r >= c0 && pad_r <= c1) && !(pad_e >= c0 && pad_e <= c1);
+    if (clean) return (1u << CPT) - 1u;
     uint32_t bits = 0u;
 #pragma unroll
     for (int kc = 0; kc < CPT; ++kc) {
