@@ -451,7 +451,7 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}, "
+        print(f"bench.py: the library runs on exactly one GPU (asked for --gpus {args.gpus}, "
               f"WORLD_SIZE {world}); problems are independent, so more GPUs would each run the "
               f"same single-GPU path on their share of heads.", file=sys.stderr)
         return 2
