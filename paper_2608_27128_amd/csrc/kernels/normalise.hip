@@ -143,6 +143,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
   const int tfirst = (bx - si.prep_blk0) * (TPB * kPrepIter) + threadIdx.x / LPT;
   const int64_t base = h * PT + si.perm_off;
   const int ret_cols = pmeta[q].ret_chunks * kChunk;
+  const int n_ret = pmeta[q].n_ret;
 
   uint4 raw[kPrepIter];
 #pragma unroll
@@ -161,8 +162,12 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
     const bool r = retained != nullptr && retained[h * T + tt] != 0;
     const int pr = prank[base + (valid ? tl : 0)];
     const int p = r ? pr : ret_cols + ((valid ? tl : 0) - pr);
-    uint16_t* dst = pkeys + (base + p) * DCOL;
     const bool copy = valid && (r || copy_evicted);  // evicted columns only for all-keys sweeps
+    // The last column of a group fills the rest of its 32-column chunk with copies of itself
+    // (key and inverse norm; the position list keeps -1 there), so that chunk holds only
+    // exact ties of a real column and the similarity sweep needs no padding test for it.
+    const int last = r ? n_ret - 1 : ret_cols + (si.len - n_ret) - 1;
+    const int fill_end = (p == last && copy) ? (p / kChunk + 1) * kChunk : p + 1;
 
     double ss = 0.0;
     if constexpr (F32) {
@@ -184,9 +189,10 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
         uint16_t* row = hilo + (h * T + tt) * (2 * D) + sub * 4;
         *reinterpret_cast<uint2*>(row) = phi;
         *reinterpret_cast<uint2*>(row + D) = plo;
-        if (copy) {
-          *reinterpret_cast<uint2*>(dst + sub * 4) = phi;
-          *reinterpret_cast<uint2*>(dst + D + sub * 4) = plo;
+        for (int k = p; copy && k < fill_end; ++k) {
+          uint16_t* dk = pkeys + (base + k) * DCOL;
+          *reinterpret_cast<uint2*>(dk + sub * 4) = phi;
+          *reinterpret_cast<uint2*>(dk + D + sub * 4) = plo;
         }
       }
     } else {
@@ -197,7 +203,8 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
         const double x1 = (double)__uint_as_float(wds[e] & 0xFFFF0000u);
         ss += x0 * x0 + x1 * x1;
       }
-      if (copy) *reinterpret_cast<uint4*>(dst + sub * 8) = raw[it];
+      for (int k = p; copy && k < fill_end; ++k)
+        *reinterpret_cast<uint4*>(pkeys + (base + k) * DCOL + sub * 8) = raw[it];
     }
 #pragma unroll
     for (int off = LPT / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, LPT);
@@ -208,7 +215,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
       else if (ss > 0.0) rv = (float)(1.0 / sqrt(ss));
       else rv = 0.0f;                                       // zero key: similarity 0 to all
       rinv[h * T + tt] = rv;
-      rcol[base + p] = rv;
+      for (int k = p; k < fill_end; ++k) rcol[base + k] = rv;
       if (bad) {
         atomicOr(&pmeta[q].flags, kFlagNonfinite);
         if (status) status[q] = 2;  // TWINKV_PROBLEM_NONFINITE

@@ -274,6 +274,14 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     const int n_ev = len - pm.n_ret;
     pad_r = (pm.n_ret % kChunk) ? pm.n_ret / kChunk : -1;
     pad_e = (n_ev % kChunk) ? (ret_pad + n_ev) / kChunk : -1;
+    if constexpr (!COUNT && FG > 1) {
+      // the key preparation fills a group's partial last chunk with copies of its last
+      // column (exact ties), so the maximum needs no padding test there; counting does,
+      // and the per-chunk configurations keep the test (it is still correct: the masked
+      // pass skips the copies by their position -1)
+      pad_r = -1;
+      pad_e = -1;
+    }
     cr_lo = __builtin_amdgcn_readfirstlane(cr_lo);
     cr_hi = __builtin_amdgcn_readfirstlane(cr_hi);
     ce_lo = __builtin_amdgcn_readfirstlane(ce_lo);
@@ -646,6 +654,9 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     for (int grp = 0; grp < 2; ++grp) {
       uint32_t v = runs[grp] & ~LOW;
       int p = cids[grp] * kChunk + slot_col(15 - (int)(runs[grp] & 15u), half);
+      // a slot past the group's last column holds a copy of that column
+      if constexpr (FG > 1)
+        p = min(p, grp == 0 ? pm.n_ret - 1 : ret_chunks * kChunk + (len - pm.n_ret) - 1);
       const uint32_t v2 = __shfl_xor(v, 32);
       const int p2 = __shfl_xor(p, 32);
       if (v2 > v || (v2 == v && p2 < p)) { v = v2; p = p2; }
