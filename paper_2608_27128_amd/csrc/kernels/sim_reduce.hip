@@ -61,7 +61,9 @@ struct Cfg {
   static constexpr int STAGE = KEY_BYTES + TN * 8;    // keys + inverse norms + positions
   static constexpr int RETIRED = NWAVES * NSUB * 64 * 8;  // S0 results parked in LDS
   static constexpr int LOADS_PER_WAVE = TN * PPC / (NWAVES * 64);  // 1-KB direct loads
-  static constexpr int VALU_PER_MFMA = (48 + KSTEPS - 1) / KSTEPS;
+  // VALU instructions the schedule places beside each MFMA: one chunk's epilogue (about 40
+  // with the tile merge, 48 with a running update per chunk) over its KSTEPS MFMAs
+  static constexpr int VALU_PER_MFMA = ((FG > 1 ? 40 : 48) + KSTEPS - 1) / KSTEPS;
   static_assert((TN * PPC) % (NWAVES * 64) == 0, "tile copy must divide evenly");
   static_assert(TN % 64 == 0, "the column tables move in 64-column (256-byte) pieces");
   static_assert(2 * (KEY_BYTES + TN * 8) + RETIRED <= 160 * 1024 / WG_PER_CU,
