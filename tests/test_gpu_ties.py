@@ -90,3 +90,41 @@ def test_exact_ties_resolve_to_smallest_position(d, dtype, with_s0):
     if with_s0:
         gpu.update(best_ret=br, arg_ret=ar)
     check_scores(gpu, orc, rows, keys[0], dtype, retained[0] if with_s0 else None, W)
+
+
+@pytest.mark.parametrize("d,dtype", [(128, "bf16"), (64, "bf16")])
+@pytest.mark.parametrize("tail", [1, 17, 31])
+def test_twin_at_last_column_of_each_group(d, dtype, tail):
+    """A row's only exact twin is the last column of its group (the last retained position
+    for b, the last evicted position for the all-keys result), with that group's last
+    32-column chunk holding `tail` real columns and padding after them: the reported
+    position is the twin's, never a padding slot."""
+    n = 1400
+    rng = np.random.default_rng(tail + d)
+    f = rng.standard_normal((1, n, d)).astype(np.float32)
+    keys = synth.bf16_bits(f) if dtype == "bf16" else f
+    n_ret = 32 * 9 + tail                               # S0: 9 full chunks + tail columns
+    last_ret = n - 60                                   # the largest retained position
+    retained = np.zeros((1, n), np.uint8)
+    retained[0, [20, last_ret]] = 1                     # row 20 retained, row 10 evicted
+    pool = np.setdiff1d(np.arange(100, last_ret), [last_ret])
+    retained[0, rng.choice(pool, n_ret - 2, replace=False)] = 1
+    assert retained.sum() == n_ret and retained[0, 10] == 0
+    last_ev = n - 1                                     # every position past last_ret is evicted
+    assert (n - n_ret) % 32 != 0                        # the evicted group ends mid-chunk too
+    # row 10 (evicted) is copied to the last retained position; row 20 (retained) to the last
+    # evicted position
+    keys[0, last_ret] = keys[0, 10]
+    keys[0, last_ev] = keys[0, 20]
+    kt = to_device(keys, dtype)
+    out = binding.nn_scores(kt, mask_to_device(retained), W)
+    ar, br = host(out["arg_ret"])[0], host(out["best_ret"])[0]
+    aa, ba = host(out["arg_all"])[0], host(out["best_all"])[0]
+    assert ar[10] == last_ret and abs(br[10] - 1.0) < 4e-5, (ar[10], br[10], last_ret)
+    assert aa[10] == last_ret and abs(ba[10] - 1.0) < 4e-5
+    assert aa[20] == last_ev and abs(ba[20] - 1.0) < 4e-5, (aa[20], ba[20], last_ev)
+    # and the whole problem against the oracle
+    rows = np.arange(n)[::3]
+    orc = oracle.nn_scores(keys[0], dtype, retained[0], W, rows=rows)
+    check_scores({"best_all": ba, "arg_all": aa, "best_ret": br, "arg_ret": ar}, orc, rows,
+                 keys[0], dtype, retained[0], W)
