@@ -291,6 +291,26 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     pad_r = __builtin_amdgcn_readfirstlane(pad_r);
     pad_e = __builtin_amdgcn_readfirstlane(pad_e);
   }
+  // With the tile merge, the band is also kept per 32-row block: a chunk is dropped and
+  // redone only for the row blocks whose own band holds it (the sweep's chunk mask is one
+  // scalar operand per chunk and row block either way).
+  constexpr bool SUB_BANDS = FG > 1;
+  int sr_lo[NSUB], sr_hi[NSUB], se_lo[NSUB], se_hi[NSUB];
+  if constexpr (SUB_BANDS) {
+    const int32_t* prk = a.prank + colbase;
+    const int ret_pad = ret_chunks * kChunk;
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) {
+      const int x0 = min(max(wrow0 + 32 * s - a.w, 0), len);
+      const int x1 = min(max(wrow0 + 32 * s + 32 + a.w, 0), len);
+      const int r0 = prk[x0], r1 = prk[x1];
+      const int e0 = ret_pad + (x0 - r0), e1 = ret_pad + (x1 - r1);
+      sr_lo[s] = __builtin_amdgcn_readfirstlane(r0 < r1 ? r0 / kChunk : 1);
+      sr_hi[s] = __builtin_amdgcn_readfirstlane(r0 < r1 ? (r1 - 1) / kChunk : 0);
+      se_lo[s] = __builtin_amdgcn_readfirstlane(e0 < e1 ? e0 / kChunk : 1);
+      se_hi[s] = __builtin_amdgcn_readfirstlane(e0 < e1 ? (e1 - 1) / kChunk : 0);
+    }
+  }
   // Result bits of the CPT chunks of a tile in the main sweep (bit k: keep chunk c0 + k).
   // Dropped: chunks the masked pass redoes, the padding-only chunks that align the S0 group,
   // and chunks past the last one.  Branch-free scalar arithmetic, so the tile body stays
@@ -301,8 +321,24 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     const bool clean = (c1 < nchunks) && !(c1 >= ret_real && c0 < ret_chunks) &&
                        !(c1 >= cr_lo && c0 <= cr_hi) && !(c1 >= ce_lo && c0 <= ce_hi) &&
                        !(pad_r >= c0 && pad_r <= c1) && !(pad_e >= c0 && pad_e <= c1);
-    if (clean) return (1u << CPT) - 1u;
+    if (clean) return SUB_BANDS ? (1u << (CPT * NSUB)) - 1u : (1u << CPT) - 1u;
     uint32_t bits = 0u;
+    if constexpr (SUB_BANDS) {
+#pragma unroll
+      for (int kc = 0; kc < CPT; ++kc) {
+        const int gc = c0 + kc;
+        const int common = (int)(gc >= nchunks) |
+                           ((int)(gc >= ret_real) & (int)(gc < ret_chunks)) |
+                           (int)(gc == pad_r) | (int)(gc == pad_e);
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb) {
+          const int drop = common | ((int)(gc >= sr_lo[sb]) & (int)(gc <= sr_hi[sb])) |
+                           ((int)(gc >= se_lo[sb]) & (int)(gc <= se_hi[sb]));
+          bits |= (uint32_t)(drop ^ 1) << (kc * NSUB + sb);
+        }
+      }
+      return bits;
+    }
 #pragma unroll
     for (int kc = 0; kc < CPT; ++kc) {
       const int gc = c0 + kc;
@@ -469,6 +505,11 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     for (int kc = 0; kc < CPT; ++kc) {
       const int gc = c0 + kc;
       const uint32_t m = 0u - ((keep >> kc) & 1u);
+      // with bands per row block, the result mask of row block sb for this chunk
+      auto mask_of = [&](int sb) -> uint32_t {
+        if constexpr (SUB_BANDS) return 0u - ((keep >> (kc * NSUB + sb)) & 1u);
+        else return m;
+      };
       float rcur[16];
       // with a single row block, chain 0 is also the last chain and carries the prefetch
       const bool pre0 = (NSUB == 1) && (kc + 1 < CPT);
@@ -499,7 +540,7 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
           if (pre)
             fc[t] = *reinterpret_cast<const bf16x8*>(st + (kc + 1) * C::CHUNK_BYTES + aoff[t]);
         }
-        reduce_into(x, rcur, gc, kc, s - 1, m);
+        reduce_into(x, rcur, gc, kc, s - 1, mask_of(s - 1));
         if (kc == CPT - 1) flush(s - 1, c0);
 #pragma unroll
         for (int i = 0; i < C::KSTEPS; ++i) {
@@ -513,7 +554,7 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
 #pragma unroll
       for (int v = 0; v < 16; ++v) prv[v] = rcur[v];
       pgc = gc;
-      pmask = m;
+      pmask = mask_of(NSUB - 1);
     }
   };
 
@@ -557,7 +598,7 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   // ---- masked pass: the chunks holding window pairs or padding next to real columns, read
   // straight from the column copy, with the window / padding test per element.  Chunks are
   // visited out of order here, so equal values keep the smaller chunk index explicitly.
-  auto masked_chunk = [&](int gc, uint32_t (&rs)[NSUB], int (&cs)[NSUB]) {
+  auto masked_chunk = [&](int gc, int grp, uint32_t (&rs)[NSUB], int (&cs)[NSUB]) {
     const int col = gc * kChunk + l32;
     bf16x8 af[C::KSTEPS];
 #pragma unroll
@@ -574,6 +615,12 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
     }
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
+      if constexpr (SUB_BANDS) {
+        // only the row blocks that dropped this chunk in the sweep
+        const bool need = grp == 0 ? (gc == pad_r || (gc >= sr_lo[s] && gc <= sr_hi[s]))
+                                   : (gc == pad_e || (gc >= se_lo[s] && gc <= se_hi[s]));
+        if (!need) continue;
+      }
       f32x16 x = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < C::KSTEPS; ++t)
@@ -603,15 +650,15 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       }
     }
   };
-  auto masked_range = [&](int l, int h, uint32_t (&rs)[NSUB], int (&cs)[NSUB]) {
+  auto masked_range = [&](int l, int h, int grp, uint32_t (&rs)[NSUB], int (&cs)[NSUB]) {
 #pragma unroll 1
     for (int gc = l; gc <= h; ++gc)
-      if (gc < nchunks) masked_chunk(gc, rs, cs);
+      if (gc < nchunks) masked_chunk(gc, grp, rs, cs);
   };
   // evicted group: the live registers
   if (active && a.want_all) {
-    masked_range(ce_lo, ce_hi, run, cid);
-    if (pad_e >= 0 && !(pad_e >= ce_lo && pad_e <= ce_hi)) masked_range(pad_e, pad_e, run, cid);
+    masked_range(ce_lo, ce_hi, 1, run, cid);
+    if (pad_e >= 0 && !(pad_e >= ce_lo && pad_e <= ce_hi)) masked_range(pad_e, pad_e, 1, run, cid);
   }
   // S0 group: the parked results
   {
@@ -624,8 +671,8 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       rcid[s] = (int)v.y;
     }
     if (active) {
-      masked_range(cr_lo, cr_hi, rr, rcid);
-      if (pad_r >= 0 && !(pad_r >= cr_lo && pad_r <= cr_hi)) masked_range(pad_r, pad_r, rr, rcid);
+      masked_range(cr_lo, cr_hi, 0, rr, rcid);
+      if (pad_r >= 0 && !(pad_r >= cr_lo && pad_r <= cr_hi)) masked_range(pad_r, pad_r, 0, rr, rcid);
     }
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) retired[s * 64 + lane] = make_uint2(rr[s], (uint32_t)rcid[s]);
