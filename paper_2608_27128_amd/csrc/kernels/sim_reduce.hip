@@ -31,8 +31,10 @@
 //    as a contraction over 3d.
 //  * Pairs inside the window and padding columns only occur in a few chunks per wave, found
 //    by scalar range tests; the sweep drops their results and a masked pass redoes them at
-//    the end.  All other chunks take a 2.5-instruction-per-element epilogue (v_fmaak,
-//    v_and_or, half a v_max3).
+//    the end (with the tile merge, per 32-row block, and the padding of a group's last
+//    chunk holds copies of its last column, so that chunk is only redone when counting).
+//    All other chunks take a 2.5-instruction-per-element epilogue (v_fmaak, v_and_or, half
+//    a v_max3).
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
