@@ -90,6 +90,24 @@ def profiled_traffic(workload: str, name: str = "repair_pass", kernel: str = "si
         return None
 
 
+def host_cpu() -> dict:
+    """The host the CPU baseline ran on: model name and the CPUs this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover - not Linux
+        usable = os.cpu_count() or 1
+    return {"cpu_model": model, "cpus_usable": usable}
+
+
 def cpu_baseline(batch, target_s: float = 15.0) -> dict:
     """The fp64 oracle on a bounded sample of the same workload: whole problems (all rows,
     both reductions) in (head, sequence) order, then a row prefix of the next one, until
@@ -124,6 +142,7 @@ def cpu_baseline(batch, target_s: float = 15.0) -> dict:
         if spent >= 0.9 * target_s:
             break
     return {"value": pairs / spent, "unit": "pairs/s", "cores": int(cores), "kind": "oracle",
+            **host_cpu(),
             "sample": f"oracle.nn_scores (both reductions, fp64), d={batch.d}: "
                       f"{'; '.join(done[:3])}{' ...' if len(done) > 3 else ''} "
                       f"({len(done)} problems), {pairs:.3e} ordered pairs in {spent:.1f} s"}
@@ -151,6 +170,7 @@ def compact_cpu_baseline(batch, values_of, s1, target_s: float = 10.0) -> dict:
         if spent >= target_s:
             break
     return {"value": nbytes / spent / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            **host_cpu(),
             "sample": f"oracle.compact_problem on {done} whole problems of {H * S} "
                       f"(keys and values, {row}-byte rows), {nbytes / 1e9:.2f} GB in {spent:.1f} s"}
 
