@@ -611,7 +611,8 @@ def main() -> int:
                            "max": float(np.max(step_ms))},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": profiled_traffic(sp.name) if args.path == "repair" else None,
+                     "traffic": profiled_traffic(sp.name, "repair_pass" if args.path == "repair"
+                                                 else f"{args.path}_pass"),
                      "kernel": "sim_reduce_kernel", "kernel_ms": k2_ms,
                      "kernel_ms_median": float(np.median(k2_each)),
                      "kernel_ms_min": float(np.min(k2_each)),
