@@ -207,8 +207,11 @@ def test_repair_from_scores_random_ties(seed):
             assert st[h, s].tolist() == [r["n_orphan"], r["n_donor"], r["m"], 0]
 
 
-@pytest.mark.parametrize("lens", [[3000, 10], [9000, 4100], [20000, 0, 17], [40000, 5]],
-                         ids=["cache4096", "cache16384", "cache32768", "uncached"])
+@pytest.mark.parametrize("lens", [[3000, 10], [4096, 7], [4097, 9], [9000, 4100], [16384, 3],
+                                  [16385, 0], [20000, 0, 17], [32768, 2], [32769, 4],
+                                  [40000, 5]],
+                         ids=["cache4096", "at4096", "past4096", "cache16384", "at16384",
+                              "past16384", "cache32768", "at32768", "past32768", "uncached"])
 def test_repair_from_scores_every_cache_size(lens):
     """The selection kernel has an LDS copy of b and S0 for sequences of up to 4096, 16384 and
     32768 tokens and reads global memory beyond that: every variant must give the oracle's

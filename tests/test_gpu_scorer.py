@@ -134,11 +134,11 @@ def test_score_evict_vs_oracle(H, lens, d, dtype, w, tau, budget_frac, n_sink, n
     assert same >= (H * len(lens)) // 2
 
 
-@pytest.mark.parametrize("n", [9000, 20000, 40000], ids=["cache16384", "cache32768", "uncached"])
+@pytest.mark.parametrize("n", [4096, 4097, 9000, 16384, 16385, 20000, 32768, 32769, 40000])
 def test_score_evict_every_cache_size(n):
     """The eviction kernel keeps an LDS copy of the counts for sequences of up to 4096, 16384
     and 32768 tokens and reads global memory beyond that; the logic replay on the GPU's own
-    counts must hold bit for bit in every variant."""
+    counts must hold bit for bit in every variant, at each limit and one token past it."""
     batch = synth.make_batch(small_spec(1, [n], 64, "bf16", 32, 7 + n % 97, dup_frac=0.3))
     budget = np.array([(3 * n) // 10], dtype=np.int64)
     gpu = binding.score_evict(to_device(batch.keys, "bf16"), budget, 0.8, 32, 4, 64,

@@ -53,6 +53,18 @@ def test_select_topk_vs_oracle(kind, lens):
     run_select(scores, lens, budgets, 4, 64)
 
 
+@pytest.mark.parametrize("n", [4096, 4097, 16384, 16385, 32768, 32769])
+@pytest.mark.parametrize("kind", ["ties", "special"])
+def test_select_topk_size_boundaries(n, kind):
+    """The longest sequence of a batch picks the selection's workgroup size and whether the
+    keys are copied to LDS (4096, 16384 and 32768 tokens): a sequence at each limit and one
+    past it, with a short sequence beside it in the same batch, bit for bit."""
+    rng = np.random.default_rng(n + len(kind))
+    lens = [n, 37]
+    scores = draw_scores(rng, 2, sum(lens), kind)
+    run_select(scores, lens, [int(rng.integers(0, n + 1)), 20], 4, 64)
+
+
 def test_select_topk_budget_edges():
     """Budget 0, below the protected count (the lowest protected positions), exactly the
     protected count, the length and beyond; protected regions covering everything."""
