@@ -249,3 +249,41 @@ def test_binding_refuses_host_tensors():
     torch = pytest.importorskip("torch")
     with pytest.raises(ValueError):
         binding.nn_scores(torch.zeros((4, 64), dtype=torch.bfloat16))
+
+
+def test_missing_library_raises(monkeypatch):
+    """No fallback: without the built library every call fails with an error naming it."""
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", os.path.join(ROOT, "no_such_dir", "libtwinkv.so"))
+    with pytest.raises(RuntimeError, match="is missing"):
+        binding.lib()
+    with pytest.raises(RuntimeError, match="is missing"):
+        binding.version()
+
+
+def test_product_package_never_reaches_the_oracle():
+    """The package (kernels, C ABI, binding, input generator, build) neither imports nor
+    loads anything under oracle/: the oracle is test infrastructure only."""
+    pkg = os.path.join(ROOT, "paper_2608_27128_amd")
+    offenders = []
+    for dirpath, _, files in os.walk(pkg):
+        if "_build" in dirpath or "__pycache__" in dirpath:
+            continue
+        for f in files:
+            if not f.endswith((".py", ".hip", ".cpp", ".h")):
+                continue
+            text = open(os.path.join(dirpath, f), errors="replace").read()
+            if re.search(r"^\s*(import\s+oracle|from\s+oracle\b)|oracle/", text, flags=re.M):
+                offenders.append(os.path.relpath(os.path.join(dirpath, f), ROOT))
+    assert offenders == []
+
+
+def test_oracle_imports_nothing_of_the_package():
+    """The oracle shares no code with the HIP path: it imports numpy and nothing else."""
+    src = os.path.join(ROOT, "oracle")
+    for f in os.listdir(src):
+        if f.endswith(".py"):
+            text = open(os.path.join(src, f)).read()
+            mods = re.findall(r"^\s*(?:from\s+(\S+)\s+import|import\s+(\S+))", text, flags=re.M)
+            names = {a or b for a, b in mods}
+            assert names <= {"numpy", "__future__", ".twinkv_oracle"}, (f, names)
