@@ -210,8 +210,9 @@ int64_t twinkv_levels_workspace_bytes(int dtype, int d, int n_heads, int n_seqs,
  * maximum score, so they are kept first; among equal scores the later position is kept
  * first (recency).  With budget >= len every token is kept; with budget 0 none.
  *
- *   budget        (host) [n_seqs] int64 >= 0: tokens to keep per problem of sequence s (the
- *                 paper's ceil((1 - rho) n) for compression ratio rho is the caller's).
+ *   budget        (host) [n_seqs] int64 in [0, 2^31 - 1]: tokens to keep per problem of
+ *                 sequence s (the paper's ceil((1 - rho) n) for compression ratio rho is the
+ *                 caller's).
  *   retained_out  [n_heads][T] uint8, receives the kept set as 0/1 (required).
  *   counts        [n_heads][T] int32, the Eq. 2 counts.  Nullable (then kept in workspace).
  *   scores        [n_heads][T] fp32, the Eq. 3 scores.  Nullable.
@@ -236,7 +237,8 @@ int twinkv_score_evict(const void* keys, int dtype, int d, int n_heads, int n_se
  * (attention mass, an expected-attention estimate, a recency score) stays on the GPU.
  *
  *   scores        [n_heads][T] fp32 (any values, NaN and infinities included).
- *   budget        (host) [n_seqs] int64 >= 0: tokens to keep per problem of sequence s.
+ *   budget        (host) [n_seqs] int64 in [0, 2^31 - 1]: tokens to keep per problem of
+ *                 sequence s (values above the length keep everything).
  *   retained_out  [n_heads][T] uint8, receives the kept set as 0/1 (required).
  *   stats         [n_heads * n_seqs][4] int32 = {tokens kept, NaN scores, 0, 0}.  Nullable.
  *   workspace     twinkv_workspace_bytes(TWINKV_OP_REPAIR_FROM_SCORES, ...) bytes (the

@@ -188,6 +188,7 @@ def test_select_topk_validation():
     assert call(ns=-1) == E_ARG
     assert call(nr=-2) == E_ARG
     assert call(budget=(10, -1)) == E_ARG
+    assert call(budget=(2 ** 31, 5)) == E_ARG       # above the documented range
     assert call(cu=(0, 100, 90)) == E_ARG           # decreasing offsets
     assert call(cu=(5, 100, 150)) == E_ARG          # first offset not 0
     assert call(wsb=0) == E_WS
