@@ -31,9 +31,12 @@
  * must be multiples of 16.  Per-token arrays (retained masks, scores, indices) are contiguous
  * [n_heads][T].  Every entry point enqueues work on `stream` (a hipStream_t passed as void*;
  * NULL = the default stream) and returns without waiting; results are valid once the stream
- * has reached that point.  The small per-sequence table built from the host arrays is copied
- * into the workspace with an asynchronous host-to-device copy from pageable memory, which
- * consumes the host data before returning.
+ * has reached that point.  The small per-sequence table built from the host arrays reaches
+ * the workspace as the kernel arguments of upload launches, so the host arrays are consumed
+ * before the call returns and no host memory is read later.  A call enqueues kernel launches
+ * only (no memset, no host copy, no allocation), so it may be captured into a HIP graph; a
+ * replay repeats the captured batch description (sequence lengths, budgets, tau, w) and
+ * re-reads the device buffers it was given.  twinkv_profile_sim_events adds event records.
  *
  * Errors.  Argument errors are detected on the host before anything is enqueued and are
  * returned synchronously (TWINKV_E_*).  A HIP failure while enqueueing returns TWINKV_E_HIP.

@@ -137,10 +137,6 @@ def _prep_keys(keys):
         keys = keys.unsqueeze(0)
     if keys.dim() != 3:
         raise ValueError("keys must be (n_heads, T, d) or (T, d)")
-    if not keys.is_cuda:
-        raise ValueError("keys must be on a GPU")
-    if keys.stride(2) != 1:
-        keys = keys.contiguous()
     if keys.dtype == torch.bfloat16:
         dt = TWINKV_BF16
     elif keys.dtype == torch.float32:
@@ -150,8 +146,57 @@ def _prep_keys(keys):
     return keys, dt
 
 
+def _on_gpu(t, name: str):
+    """Device check, after the shape and offset checks (which need no GPU)."""
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a GPU")
+    if t.dim() == 3 and t.stride(2) != 1:
+        t = t.contiguous()
+    return t
+
+
+def _vec2d(x, name: str):
+    """A float32 (n_heads, T) or (T,) tensor, before the device check."""
+    torch = _torch()
+    if x.dim() == 1:
+        x = x.unsqueeze(0)
+    if x.dim() != 2 or x.dtype != torch.float32:
+        raise ValueError(f"{name} must be a float32 (n_heads, T) tensor")
+    return x
+
+
 def _cu(cu_seqlens, T: int):
-    return np.array([0, T], dtype=np.int64) if cu_seqlens is None else np.asarray(cu_seqlens, dtype=np.int64)
+    """The sequence offsets as int64, checked against the tensors' token count T: the library
+    lays every [n_heads][T] buffer out from cu_seqlens, so an offset list that ends anywhere
+    but T would make its kernels read or write outside the tensors."""
+    if cu_seqlens is None:
+        return np.array([0, T], dtype=np.int64)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    if cu.ndim != 1 or len(cu) < 2:
+        raise ValueError("cu_seqlens must list n_seqs + 1 >= 2 offsets")
+    if cu[0] != 0 or np.any(np.diff(cu) < 0):
+        raise ValueError("cu_seqlens must start at 0 and never decrease")
+    if cu[-1] != T:
+        raise ValueError(f"cu_seqlens[-1] = {int(cu[-1])} must equal T = {T}")
+    return cu
+
+
+def _check_outputs(out: dict, spec: dict, fn: str) -> dict:
+    """Buffers passed back through ``outputs``: each present entry must have the shape, dtype
+    and device the call writes (``spec``: name -> (shape, dtype, device, required))."""
+    got = dict(out)
+    for name, (shape, dtype, dev, required) in spec.items():
+        t = got.get(name)
+        if t is None:
+            if required:
+                raise ValueError(f"{fn}: outputs[{name!r}] is required")
+            continue
+        if tuple(t.shape) != tuple(shape) or t.dtype != dtype or t.device != dev:
+            raise ValueError(f"{fn}: outputs[{name!r}] must be {tuple(shape)} {dtype} on {dev}, "
+                             f"got {tuple(t.shape)} {t.dtype} on {t.device}")
+        if not t.is_contiguous():
+            raise ValueError(f"{fn}: outputs[{name!r}] must be contiguous")
+    return got
 
 
 def _ptr(t) -> Optional[int]:
@@ -180,6 +225,13 @@ def _mask(x, n_heads, T, device, name):
     return x.contiguous()
 
 
+def _workspace(workspace, nbytes: int, dev):
+    torch = _torch()
+    if workspace is not None and workspace.numel() >= nbytes:
+        return workspace
+    return torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+
+
 def nn_scores(keys, retained=None, w: int = 32, cu_seqlens=None, *, want_arg: bool = True,
               workspace=None) -> dict:
     """Best twin of every token: best_all/arg_all over all keys, best_ret/arg_ret (Eq. 4 b_i(S0))
@@ -187,10 +239,9 @@ def nn_scores(keys, retained=None, w: int = 32, cu_seqlens=None, *, want_arg: bo
     torch = _torch()
     keys, dt = _prep_keys(keys)
     H, T, d = keys.shape
-    dev = keys.device
     cu = _cu(cu_seqlens, T)
-    if cu[-1] != T:
-        raise ValueError("cu_seqlens[-1] must equal T")
+    keys = _on_gpu(keys, "keys")
+    dev = keys.device
     ret = _mask(retained, H, T, dev, "retained")
     out = {
         "best_all": torch.empty((H, T), dtype=torch.float32, device=dev),
@@ -200,12 +251,9 @@ def nn_scores(keys, retained=None, w: int = 32, cu_seqlens=None, *, want_arg: bo
     if ret is not None:
         out["best_ret"] = torch.empty((H, T), dtype=torch.float32, device=dev)
         out["arg_ret"] = torch.empty((H, T), dtype=torch.int32, device=dev) if want_arg else None
-    nbytes = workspace_bytes(OP_NN_SCORES, dt, d, H, cu)
-    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
-        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
-    cu_c = _i64_array(cu)
+    ws = _workspace(workspace, workspace_bytes(OP_NN_SCORES, dt, d, H, cu), dev)
     rc = lib().twinkv_nn_scores(
-        keys.data_ptr(), dt, d, H, len(cu) - 1, cu_c, keys.stride(0), keys.stride(1),
+        keys.data_ptr(), dt, d, H, len(cu) - 1, _i64_array(cu), keys.stride(0), keys.stride(1),
         _ptr(ret), int(w), _ptr(out["best_all"]), _ptr(out["arg_all"]),
         _ptr(out.get("best_ret")), _ptr(out.get("arg_ret")), _ptr(out["status"]),
         ws.data_ptr(), ws.numel(), _stream(dev))
@@ -224,36 +272,47 @@ def nn_scores_levels(keys, level, n_levels: int, w: int = 32, cu_seqlens=None, *
     torch = _torch()
     keys, dt = _prep_keys(keys)
     H, T, d = keys.shape
-    dev = keys.device
     cu = _cu(cu_seqlens, T)
-    if cu[-1] != T:
-        raise ValueError("cu_seqlens[-1] must equal T")
     n_seqs = len(cu) - 1
-    lv = _mask(level, H, T, dev, "level")
-    if lv is None:
+    if level is None:
         raise ValueError("level is required")
+    if not 1 <= int(n_levels) <= MAX_LEVELS:
+        raise ValueError(f"n_levels must be in [1, {MAX_LEVELS}]")
+    keys = _on_gpu(keys, "keys")
+    dev = keys.device
+    lv = _mask(level, H, T, dev, "level")
+    f32, i32 = torch.float32, torch.int32
+    spec = {
+        "best_lvl": ((n_levels, H, T), f32, dev, True),
+        "arg_lvl": ((n_levels, H, T), i32, dev, False),
+        "best_all": ((H, T), f32, dev, False),
+        "arg_all": ((H, T), i32, dev, False),
+        "status": ((H * n_seqs,), i32, dev, True),
+    }
     if outputs is None:
         out = {
-            "best_lvl": torch.empty((n_levels, H, T), dtype=torch.float32, device=dev),
-            "arg_lvl": torch.empty((n_levels, H, T), dtype=torch.int32, device=dev) if want_arg else None,
-            "best_all": torch.empty((H, T), dtype=torch.float32, device=dev) if want_all else None,
-            "arg_all": torch.empty((H, T), dtype=torch.int32, device=dev) if (want_all and want_arg) else None,
-            "status": torch.empty((H * n_seqs,), dtype=torch.int32, device=dev),
+            "best_lvl": torch.empty((n_levels, H, T), dtype=f32, device=dev),
+            "arg_lvl": torch.empty((n_levels, H, T), dtype=i32, device=dev) if want_arg else None,
+            "best_all": torch.empty((H, T), dtype=f32, device=dev) if want_all else None,
+            "arg_all": torch.empty((H, T), dtype=i32, device=dev) if (want_all and want_arg) else None,
+            "status": torch.empty((H * n_seqs,), dtype=i32, device=dev),
         }
     else:
-        out = dict(outputs)
-    cu_c = _i64_array(cu)
-    nbytes = levels_workspace_bytes(dt, d, H, cu, n_levels, want_all)
-    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
-        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+        out = _check_outputs(outputs, spec, "nn_scores_levels")
+        want_all = out.get("best_all") is not None or out.get("arg_all") is not None
+    ws = _workspace(workspace, levels_workspace_bytes(dt, d, H, cu, n_levels, want_all), dev)
     rc = lib().twinkv_nn_scores_levels(
-        keys.data_ptr(), dt, d, H, n_seqs, cu_c, keys.stride(0), keys.stride(1), lv.data_ptr(),
-        int(n_levels), int(w), _ptr(out.get("best_all")), _ptr(out.get("arg_all")),
+        keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
+        lv.data_ptr(), int(n_levels), int(w), _ptr(out.get("best_all")), _ptr(out.get("arg_all")),
         out["best_lvl"].data_ptr(), _ptr(out.get("arg_lvl")), _ptr(out["status"]),
         ws.data_ptr(), ws.numel(), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_nn_scores_levels", rc)
     return {k: v for k, v in out.items() if v is not None}
+
+
+def _budget(budget, n_seqs: int):
+    return np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,)).copy()
 
 
 def repair(keys, retained, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent: int = 64,
@@ -263,38 +322,45 @@ def repair(keys, retained, budget, tau: float, w: int = 32, n_sink: int = 4, n_r
     and the scores it was computed from (best_ret = b; best_all/arg_all when want_all).
 
     ``outputs`` may pass back the dict of an earlier call with the same shapes to reuse its
-    buffers; ``out_mask`` may be ``retained`` itself for an in-place update."""
+    buffers (the entries it holds decide what is computed); ``out_mask`` may be ``retained``
+    itself for an in-place update."""
     torch = _torch()
     keys, dt = _prep_keys(keys)
     H, T, d = keys.shape
-    dev = keys.device
     cu = _cu(cu_seqlens, T)
     n_seqs = len(cu) - 1
-    ret = _mask(retained, H, T, dev, "retained")
-    if ret is None:
+    if retained is None:
         raise ValueError("retained is required")
-    bud = np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,)).copy()
+    bud = _budget(budget, n_seqs)
+    keys = _on_gpu(keys, "keys")
+    dev = keys.device
+    ret = _mask(retained, H, T, dev, "retained")
+    f32, i32 = torch.float32, torch.int32
     if outputs is None:
-        def f32():
-            return torch.empty((H, T), dtype=torch.float32, device=dev)
-
-        def i32():
-            return torch.empty((H, T), dtype=torch.int32, device=dev)
         out = {
             "s1": torch.empty((H, T), dtype=torch.uint8, device=dev),
-            "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
-            "best_ret": f32(),
-            "arg_ret": i32() if want_arg else None,
-            "best_all": f32() if want_all else None,
-            "arg_all": i32() if (want_all and want_arg) else None,
+            "stats": torch.empty((H * n_seqs, 4), dtype=i32, device=dev),
+            "best_ret": torch.empty((H, T), dtype=f32, device=dev),
+            "arg_ret": torch.empty((H, T), dtype=i32, device=dev) if want_arg else None,
+            "best_all": torch.empty((H, T), dtype=f32, device=dev) if want_all else None,
+            "arg_all": torch.empty((H, T), dtype=i32, device=dev) if (want_all and want_arg) else None,
         }
     else:
-        out = dict(outputs)
+        spec = {
+            "s1": ((H, T), torch.uint8, dev, out_mask is None),
+            "stats": ((H * n_seqs, 4), i32, dev, True),
+            "best_ret": ((H, T), f32, dev, False),
+            "arg_ret": ((H, T), i32, dev, False),
+            "best_all": ((H, T), f32, dev, False),
+            "arg_all": ((H, T), i32, dev, False),
+        }
+        out = _check_outputs(outputs, spec, "repair")
     if out_mask is not None:
+        m = _mask(out_mask, H, T, dev, "out_mask")
+        if m.data_ptr() != out_mask.data_ptr():
+            raise ValueError("out_mask must be a contiguous uint8 (n_heads, T) tensor")
         out["s1"] = out_mask
-    nbytes = workspace_bytes(OP_REPAIR, dt, d, H, cu)
-    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
-        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace, workspace_bytes(OP_REPAIR, dt, d, H, cu), dev)
     rc = lib().twinkv_repair(
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         ret.data_ptr(), out["s1"].data_ptr(), _i64_array(bud), float(tau), int(w), int(n_sink),
@@ -309,23 +375,24 @@ def repair_from_scores(b, retained, budget, tau: float, n_sink: int = 4, n_recen
                        cu_seqlens=None, *, out_mask=None) -> dict:
     """Classification, ranking and swap of Sec. 3.4 from given scores b (n_heads, T) float32."""
     torch = _torch()
-    if b.dim() == 1:
-        b = b.unsqueeze(0)
-    if b.dtype != torch.float32 or not b.is_cuda:
-        raise ValueError("b must be a float32 GPU tensor")
-    b = b.contiguous()
+    b = _vec2d(b, "b")
     H, T = b.shape
-    dev = b.device
     cu = _cu(cu_seqlens, T)
     n_seqs = len(cu) - 1
-    ret = _mask(retained, H, T, dev, "retained")
-    if ret is None:
+    if retained is None:
         raise ValueError("retained is required")
-    bud = np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,)).copy()
-    s1 = out_mask if out_mask is not None else torch.empty((H, T), dtype=torch.uint8, device=dev)
+    bud = _budget(budget, n_seqs)
+    b = _on_gpu(b, "b").contiguous()
+    dev = b.device
+    ret = _mask(retained, H, T, dev, "retained")
+    if out_mask is not None:
+        s1 = _mask(out_mask, H, T, dev, "out_mask")
+        if s1.data_ptr() != out_mask.data_ptr():
+            raise ValueError("out_mask must be a contiguous uint8 (n_heads, T) tensor")
+    else:
+        s1 = torch.empty((H, T), dtype=torch.uint8, device=dev)
     stats = torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev)
-    nbytes = workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu)
-    ws = torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    ws = _workspace(None, workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu), dev)
     rc = lib().twinkv_repair_from_scores(
         b.data_ptr(), ret.data_ptr(), s1.data_ptr(), H, n_seqs, _i64_array(cu), _i64_array(bud),
         float(tau), int(n_sink), int(n_recent), stats.data_ptr(), ws.data_ptr(), ws.numel(),
@@ -340,15 +407,12 @@ def twin_counts(keys, tau: float, w: int = 32, cu_seqlens=None, *, workspace=Non
     torch = _torch()
     keys, dt = _prep_keys(keys)
     H, T, d = keys.shape
-    dev = keys.device
     cu = _cu(cu_seqlens, T)
-    if cu[-1] != T:
-        raise ValueError("cu_seqlens[-1] must equal T")
+    keys = _on_gpu(keys, "keys")
+    dev = keys.device
     counts = torch.empty((H, T), dtype=torch.int32, device=dev)
     status = torch.empty((H * (len(cu) - 1),), dtype=torch.int32, device=dev)
-    nbytes = workspace_bytes(OP_TWIN_COUNTS, dt, d, H, cu)
-    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
-        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace, workspace_bytes(OP_TWIN_COUNTS, dt, d, H, cu), dev)
     rc = lib().twinkv_twin_counts(
         keys.data_ptr(), dt, d, H, len(cu) - 1, _i64_array(cu), keys.stride(0), keys.stride(1),
         float(tau), int(w), counts.data_ptr(), status.data_ptr(), ws.data_ptr(), ws.numel(),
@@ -367,10 +431,11 @@ def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent
     torch = _torch()
     keys, dt = _prep_keys(keys)
     H, T, d = keys.shape
-    dev = keys.device
     cu = _cu(cu_seqlens, T)
     n_seqs = len(cu) - 1
-    bud = np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,)).copy()
+    bud = _budget(budget, n_seqs)
+    keys = _on_gpu(keys, "keys")
+    dev = keys.device
     if outputs is None:
         out = {
             "retained": torch.empty((H, T), dtype=torch.uint8, device=dev),
@@ -379,11 +444,15 @@ def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent
             "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
         }
     else:
-        out = dict(outputs)
+        spec = {
+            "retained": ((H, T), torch.uint8, dev, True),
+            "counts": ((H, T), torch.int32, dev, True),
+            "scores": ((H, T), torch.float32, dev, False),
+            "stats": ((H * n_seqs, 4), torch.int32, dev, True),
+        }
+        out = _check_outputs(outputs, spec, "score_evict")
         out.setdefault("scores", None)
-    nbytes = workspace_bytes(OP_SCORE_EVICT, dt, d, H, cu)
-    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
-        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace, workspace_bytes(OP_SCORE_EVICT, dt, d, H, cu), dev)
     rc = lib().twinkv_score_evict(
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         _i64_array(bud), float(tau), int(w), int(n_sink), int(n_recent),
@@ -401,25 +470,23 @@ def select_topk(scores, budget, n_sink: int = 4, n_recent: int = 64, cu_seqlens=
     scores: float32 (n_heads, T) on the GPU.  Returns retained uint8 (n_heads, T) and
     stats int32 (n_heads * n_seqs, 4) = {kept, NaN scores, 0, 0}."""
     torch = _torch()
-    if scores.dim() == 1:
-        scores = scores.unsqueeze(0)
-    if scores.dtype != torch.float32 or not scores.is_cuda:
-        raise ValueError("scores must be a float32 GPU tensor")
-    scores = scores.contiguous()
+    scores = _vec2d(scores, "scores")
     H, T = scores.shape
-    dev = scores.device
     cu = _cu(cu_seqlens, T)
-    if cu[-1] != T:
-        raise ValueError("cu_seqlens[-1] must equal T")
     n_seqs = len(cu) - 1
-    bud = np.broadcast_to(np.asarray(budget, dtype=np.int64), (n_seqs,))
-    out = outputs if outputs is not None else {
-        "retained": torch.empty((H, T), dtype=torch.uint8, device=dev),
-        "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
-    }
-    nbytes = workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu)
-    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
-        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    bud = _budget(budget, n_seqs)
+    scores = _on_gpu(scores, "scores").contiguous()
+    dev = scores.device
+    if outputs is None:
+        out = {
+            "retained": torch.empty((H, T), dtype=torch.uint8, device=dev),
+            "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
+        }
+    else:
+        spec = {"retained": ((H, T), torch.uint8, dev, True),
+                "stats": ((H * n_seqs, 4), torch.int32, dev, True)}
+        out = _check_outputs(outputs, spec, "select_topk")
+    ws = _workspace(workspace, workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu), dev)
     rc = lib().twinkv_select_topk(
         scores.data_ptr(), H, n_seqs, _i64_array(cu), _i64_array(bud), int(n_sink),
         int(n_recent), out["retained"].data_ptr(), _ptr(out["stats"]), ws.data_ptr(),
@@ -433,19 +500,17 @@ def prevalence(best_all, taus, cu_seqlens=None) -> "torch.Tensor":
     """Tokens with at least one twin (best_all > tau) per problem and threshold:
     int32 (n_heads * n_seqs, len(taus))."""
     torch = _torch()
-    if best_all.dim() == 1:
-        best_all = best_all.unsqueeze(0)
-    if best_all.dtype != torch.float32 or not best_all.is_cuda:
-        raise ValueError("best_all must be a float32 GPU tensor")
-    best_all = best_all.contiguous()
+    best_all = _vec2d(best_all, "best_all")
     H, T = best_all.shape
-    dev = best_all.device
     cu = _cu(cu_seqlens, T)
     n_seqs = len(cu) - 1
-    tv = np.ascontiguousarray(np.asarray(taus, dtype=np.float32))
+    tv = np.ascontiguousarray(np.asarray(taus, dtype=np.float32).reshape(-1))
+    if not 1 <= len(tv) <= MAX_TAUS:
+        raise ValueError(f"between 1 and {MAX_TAUS} thresholds")
+    best_all = _on_gpu(best_all, "best_all").contiguous()
+    dev = best_all.device
     out = torch.empty((H * n_seqs, len(tv)), dtype=torch.int32, device=dev)
-    nbytes = workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu)
-    ws = torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+    ws = _workspace(None, workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu), dev)
     rc = lib().twinkv_prevalence(
         best_all.data_ptr(), H, n_seqs, _i64_array(cu),
         tv.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(tv), out.data_ptr(),
@@ -465,23 +530,24 @@ def compact(keys, retained, capacity, values=None, cu_seqlens=None, *, want_pos:
     torch = _torch()
     keys, dt = _prep_keys(keys)
     H, T, d = keys.shape
-    dev = keys.device
     if values is not None:
         if values.dim() == 2:
             values = values.unsqueeze(0)
-        if values.dtype != keys.dtype or tuple(values.shape) != (H, T, d) or values.device != dev:
-            raise ValueError("values must match keys in dtype, shape and device")
-        if values.stride(2) != 1:
-            values = values.contiguous()
+        if values.dtype != keys.dtype or tuple(values.shape) != (H, T, d):
+            raise ValueError("values must match keys in dtype and shape")
     cu = _cu(cu_seqlens, T)
-    if cu[-1] != T:
-        raise ValueError("cu_seqlens[-1] must equal T")
     n_seqs = len(cu) - 1
-    ret = _mask(retained, H, T, dev, "retained")
-    if ret is None:
+    if retained is None:
         raise ValueError("retained is required")
-    cap = np.broadcast_to(np.asarray(capacity, dtype=np.int64), (n_seqs,)).copy()
+    cap = _budget(capacity, n_seqs)
     C = int(cap.sum())
+    keys = _on_gpu(keys, "keys")
+    dev = keys.device
+    if values is not None:
+        values = _on_gpu(values, "values")
+        if values.device != dev:
+            raise ValueError("values must be on the keys' device")
+    ret = _mask(retained, H, T, dev, "retained")
     if outputs is None:
         out = {
             "keys": torch.empty((H, C, d), dtype=keys.dtype, device=dev),
@@ -490,12 +556,18 @@ def compact(keys, retained, capacity, values=None, cu_seqlens=None, *, want_pos:
             "stats": torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev),
         }
     else:
-        out = dict(outputs)
+        spec = {
+            "keys": ((H, C, d), keys.dtype, dev, True),
+            "values": ((H, C, d), keys.dtype, dev, values is not None),
+            "pos": ((H, C), torch.int32, dev, False),
+            "stats": ((H * n_seqs, 4), torch.int32, dev, True),
+        }
+        out = _check_outputs(outputs, spec, "compact")
         out.setdefault("values", None)
         out.setdefault("pos", None)
-    nbytes = workspace_bytes(OP_COMPACT, dt, d, H, cu)
-    ws = workspace if workspace is not None and workspace.numel() >= nbytes else \
-        torch.empty((nbytes,), dtype=torch.uint8, device=dev)
+        if values is None:
+            out["values"] = None
+    ws = _workspace(workspace, workspace_bytes(OP_COMPACT, dt, d, H, cu), dev)
     vs = (values.stride(0), values.stride(1)) if values is not None else (0, 0)
     rc = lib().twinkv_compact(
         keys.data_ptr(), _ptr(values), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0),

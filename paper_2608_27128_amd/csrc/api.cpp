@@ -182,8 +182,7 @@ int prepare_scores(const void* keys, int dtype, int d, const Batch& bt, const in
 
   SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
   P.seqtab = dtab;
-  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
-                     (hipStream_t)stream) != hipSuccess)
+  if (launch_upload(tab.data(), sizeof(SeqInfo) * tab.size(), dtab, stream) != 0)
     return TWINKV_E_HIP;
 
   float* rinv = reinterpret_cast<float*>(ws + L.rinv);
@@ -388,8 +387,7 @@ int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_
   int tiles = 0;
   std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, budget, 0, tiles);
   SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
-  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
-                     (hipStream_t)stream) != hipSuccess)
+  if (launch_upload(tab.data(), sizeof(SeqInfo) * tab.size(), dtab, stream) != 0)
     return TWINKV_E_HIP;
   RepairArgs ra;
   ra.b = b;
@@ -487,8 +485,7 @@ int twinkv_select_topk(const float* scores, int n_heads, int n_seqs, const int64
   int tiles = 0;
   std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, budget, 0, tiles);
   SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
-  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
-                     (hipStream_t)stream) != hipSuccess)
+  if (launch_upload(tab.data(), sizeof(SeqInfo) * tab.size(), dtab, stream) != 0)
     return TWINKV_E_HIP;
   EvictArgs ea;
   ea.counts = nullptr;
@@ -521,8 +518,7 @@ int twinkv_prevalence(const float* best_all, int n_heads, int n_seqs, const int6
   int tiles = 0;
   std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, nullptr, 0, tiles);
   SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
-  if (hipMemcpyAsync(dtab, tab.data(), sizeof(SeqInfo) * tab.size(), hipMemcpyHostToDevice,
-                     (hipStream_t)stream) != hipSuccess)
+  if (launch_upload(tab.data(), sizeof(SeqInfo) * tab.size(), dtab, stream) != 0)
     return TWINKV_E_HIP;
   PrevalenceArgs pa;
   pa.best = best_all;
@@ -673,9 +669,7 @@ int twinkv_compact(const void* keys, const void* values, int dtype, int d, int n
     out += capacity[s];
     ck += nc;
   }
-  if (hipMemcpyAsync(ws + L.seqtab, host.data(), tab_bytes, hipMemcpyHostToDevice,
-                     (hipStream_t)stream) != hipSuccess)
-    return TWINKV_E_HIP;
+  if (launch_upload(host.data(), tab_bytes, ws + L.seqtab, stream) != 0) return TWINKV_E_HIP;
 
   const int64_t esz = dtype == TWINKV_F32 ? 4 : 2;
   CompactArgs a;

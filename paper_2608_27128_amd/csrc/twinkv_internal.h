@@ -49,6 +49,11 @@ struct Layout {
 // ---- launchers (defined in the kernel translation units) ----
 // Each returns 0 on success or a hipError_t value.
 
+// Copies `bytes` (a multiple of 4) of host memory to device memory `dst` on `stream` through
+// kernel arguments: the host buffer may be freed as soon as the call returns, also when the
+// launches are captured into a graph.
+int launch_upload(const void* src, size_t bytes, void* dst, void* stream);
+
 // K1a: stable partition of each problem's positions into [S0 | evicted] column lists from the
 // retained mask: pcol (positions, -1 for padding), prank[t] = number of S0 positions before t
 // (t = 0..len), the per-problem meta, rcol = 0 at padding, status = 0.

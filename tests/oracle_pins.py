@@ -303,6 +303,26 @@ def pin_twin_counts_golden(o):
                                   st["counts_at_0.4999"])
 
 
+def pin_twin_counts_band(o):
+    """The margin band the count parity tests rely on: counts at tau + margin and at
+    tau - margin, window respected, strict comparisons (hand-derived, exact arithmetic)."""
+    fx = _load("twin_counts.json")
+    st, band = fx["strict"], fx["band"]
+    K = np.asarray(st["keys"], dtype=np.float32)
+    for case in band["cases"]:
+        r = o.twin_counts(K, "f32", case["tau"], st["w"], margin=case["margin"])
+        for key in ("counts", "counts_lo", "counts_hi"):
+            np.testing.assert_array_equal(r[key], case[key], err_msg=f"{key} at tau {case['tau']}")
+    # the band is ordered and collapses to the counts at margin 0+
+    rng = np.random.default_rng(13)
+    K = rng.standard_normal((60, 8)).astype(np.float32)
+    K[30:45] = K[5:20] + np.float32(0.05) * rng.standard_normal((15, 8)).astype(np.float32)
+    r = o.twin_counts(K, "f32", 0.8, 3, margin=0.05)
+    assert np.all(r["counts_lo"] <= r["counts"]) and np.all(r["counts"] <= r["counts_hi"])
+    assert np.any(r["counts_lo"] < r["counts_hi"])
+    assert "counts_lo" not in o.twin_counts(K, "f32", 0.8, 3)
+
+
 def _brute_counts(K, tau, w):
     """Pure-Python Eq. 2 on a tiny input: its own normalisation and dot products."""
     import math
@@ -519,7 +539,7 @@ ALL_PINS = [
     pin_nonfinite_rejected, pin_repair_ranked, pin_oscillation, pin_repair_invariants,
     pin_exact_noops, pin_redundancy_consistent_noop, pin_second_pass_condition,
     pin_budget_checked,
-    pin_twin_counts_golden, pin_twin_counts_brute_force, pin_twin_counts_vs_best,
+    pin_twin_counts_golden, pin_twin_counts_band, pin_twin_counts_brute_force, pin_twin_counts_vs_best,
     pin_scores_eq3, pin_evict_golden, pin_evict_invariants, pin_prevalence_golden,
     pin_compact_golden, pin_compact_invariants, pin_exemption_diagnostics,
     pin_select_golden, pin_select_brute_force, pin_select_invariants,

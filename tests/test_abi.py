@@ -252,6 +252,66 @@ def test_binding_refuses_host_tensors():
         binding.nn_scores(torch.zeros((4, 64), dtype=torch.bfloat16))
 
 
+def _no_library(monkeypatch):
+    """Any call that reaches the library fails the test: the checks below must come first."""
+    def boom():
+        raise AssertionError("the wrapper reached the library")
+    monkeypatch.setattr(binding, "lib", boom)
+
+
+@pytest.mark.parametrize("cu", [(0, 40), (0, 80), (0, 30, 70), (0, 70, 64), (5, 64), (64,)])
+def test_binding_checks_cu_seqlens_against_T(monkeypatch, cu):
+    """Every wrapper refuses offsets that do not end at the tensors' T (64 tokens here), or
+    that decrease or do not start at 0, before it calls the library: the library lays each
+    [n_heads][T] buffer out from cu_seqlens."""
+    torch = pytest.importorskip("torch")
+    _no_library(monkeypatch)
+    H, T, d = 2, 64, 64
+    keys = torch.zeros((H, T, d), dtype=torch.bfloat16)
+    mask = torch.zeros((H, T), dtype=torch.uint8)
+    f = torch.zeros((H, T), dtype=torch.float32)
+    n_seqs = max(1, len(cu) - 1)
+    calls = {
+        "nn_scores": lambda: binding.nn_scores(keys, mask, 32, cu),
+        "nn_scores_levels": lambda: binding.nn_scores_levels(keys, mask, 1, 32, cu),
+        "repair": lambda: binding.repair(keys, mask, [0] * n_seqs, 0.9, 32, 4, 4, cu),
+        "repair_from_scores": lambda: binding.repair_from_scores(f, mask, [0] * n_seqs, 0.9, 4, 4, cu),
+        "twin_counts": lambda: binding.twin_counts(keys, 0.9, 32, cu),
+        "score_evict": lambda: binding.score_evict(keys, [0] * n_seqs, 0.9, 32, 4, 4, cu),
+        "select_topk": lambda: binding.select_topk(f, [0] * n_seqs, 4, 4, cu),
+        "prevalence": lambda: binding.prevalence(f, [0.9], cu),
+        "compact": lambda: binding.compact(keys, mask, [0] * n_seqs, cu_seqlens=cu),
+    }
+    for name, call in calls.items():
+        with pytest.raises(ValueError, match="cu_seqlens"):
+            call()
+
+
+def test_binding_checks_passed_outputs(monkeypatch):
+    """Buffers passed back through `outputs` are checked against the shapes the call writes
+    (the device check comes first, so on a CPU-only host the call stops there, and the shape
+    check itself is exercised directly)."""
+    torch = pytest.importorskip("torch")
+    _no_library(monkeypatch)
+    dev = torch.device("cpu")
+    good = {"s1": torch.zeros((2, 8), dtype=torch.uint8), "stats": torch.zeros((2, 4), dtype=torch.int32)}
+    spec = {"s1": ((2, 8), torch.uint8, dev, True), "stats": ((2, 4), torch.int32, dev, True),
+            "best_ret": ((2, 8), torch.float32, dev, False)}
+    assert set(binding._check_outputs(good, spec, "repair")) == {"s1", "stats"}
+    with pytest.raises(ValueError, match="s1"):
+        binding._check_outputs({**good, "s1": torch.zeros((2, 9), dtype=torch.uint8)}, spec, "repair")
+    with pytest.raises(ValueError, match="best_ret"):
+        binding._check_outputs({**good, "best_ret": torch.zeros((2, 8), dtype=torch.float64)}, spec, "repair")
+    with pytest.raises(ValueError, match="stats"):
+        binding._check_outputs({"s1": good["s1"]}, spec, "repair")
+    with pytest.raises(ValueError, match="contiguous"):
+        binding._check_outputs({**good, "s1": torch.zeros((8, 2), dtype=torch.uint8).t()}, spec, "repair")
+    # with valid offsets the wrappers stop at the device check on a host tensor
+    keys = torch.zeros((2, 8, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        binding.repair(keys, good["s1"], 0, 0.9, 32, 4, 4, (0, 8), outputs=good)
+
+
 def test_missing_library_raises(monkeypatch):
     """No fallback: without the built library every call fails with an error naming it."""
     monkeypatch.setattr(binding, "_lib", None)

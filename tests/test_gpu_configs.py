@@ -1,16 +1,25 @@
 """The five workloads at their full sizes, in the launch configuration bench.py times.
 
-The GPU processes every problem of each workload in one call.  The oracle checks sampled
-rows of sampled problems (each row costs O(N d)), complete problems where a full O(N^2 d)
-oracle pass is affordable, and properties that must hold for every problem at any size."""
+The GPU processes every problem of each workload in one call.  On every problem the oracle
+replays the repair logic of Sec. 3.4 on the GPU's own scores (bit for bit) and checks the
+set's properties; complete problems go through the full O(N^2 d) oracle and the token-by-token
+protocol of gpu_util; sampled rows of further problems check both reductions.  Each workload's
+exemption accounting (rows exempt by the runner-up margin, flags within the tolerance of tau,
+tokens at a selection cut) is printed and, with TWINKV_PARITY_RECORD set, recorded."""
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 
 import oracle
-from gpu_util import check_repair, check_scores, host, mask_to_device, to_device
+from gpu_util import (check_repair, check_scores, host, mask_to_device, merge_repairs,
+                      merge_scores, record_exemptions, replay_repair, to_device)
 from paper_2608_27128_amd import binding, synth
 
 pytestmark = pytest.mark.gpu
+
+# complete problems run through the oracle concurrently (numpy releases the GIL)
+ORACLE_THREADS = 4
 
 
 def sample_rows(n, rng, k=192, rb=512):
@@ -21,7 +30,9 @@ def sample_rows(n, rng, k=192, rb=512):
 
 
 def check_all_problems(batch, out, tau, n_sink, n_recent):
-    """Properties of every problem's result (budget, swap count, membership, protection)."""
+    """Every problem: the oracle's Sec. 3.4 logic replayed on the GPU's own b gives the GPU's
+    S1 and (|O|, |D|, m) bit for bit (so severity order, tie rule, budget, membership and
+    protection all hold); returns the swaps made."""
     s1 = host(out["s1"])
     b = host(out["best_ret"])
     st = host(out["stats"]).reshape(batch.n_heads, batch.n_seqs, 4)
@@ -29,62 +40,60 @@ def check_all_problems(batch, out, tau, n_sink, n_recent):
     swapped = 0
     for s in range(batch.n_seqs):
         a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
-        n = e - a
-        s0 = batch.retained[:, a:e].astype(bool)
-        s1s = s1[:, a:e].astype(bool)
-        bb = b[:, a:e]
-        idx = np.arange(n)
-        prot = (idx < n_sink) | (idx >= n - n_recent)
-        O = ~s0 & (bb < tau)
-        D = s0 & ~prot[None, :] & (bb >= tau)
-        m = np.minimum(O.sum(1), D.sum(1))
-        assert np.all(s1s.sum(1) == batch.budget[s])
-        assert np.all(st[:, s, 0] == O.sum(1)) and np.all(st[:, s, 1] == D.sum(1))
-        assert np.all(st[:, s, 2] == m)
-        adm, ev = s1s & ~s0, s0 & ~s1s
-        assert np.all(adm.sum(1) == m) and np.all(ev.sum(1) == m)
-        assert not (adm & ~O).any() and not (ev & ~D).any()
-        assert not (s0 & prot[None, :] & ~s1s).any()
-        swapped += int(m.sum())
+        for h in range(batch.n_heads):
+            s0 = batch.retained[h, a:e]
+            r = replay_repair(s1[h, a:e], st[h, s], b[h, a:e], s0, tau, n_sink, n_recent)
+            assert int(s1[h, a:e].sum()) == int(batch.budget[s])
+            swapped += r["m"]
     return swapped
 
 
-def check_sampled_rows(batch, out, problems, rng, w):
-    agg = {}
+def check_sampled_rows(batch, out, problems, rng, w, agg=None):
+    agg = {} if agg is None else agg
     for (h, s) in problems:
         a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
         k, r = batch.keys[h, a:e], batch.retained[h, a:e]
         rows = sample_rows(e - a, rng)
         orc = oracle.nn_scores(k, batch.dtype, r, w, rows=rows)
         g = {key: host(out[key][h, a:e]) for key in ("best_all", "arg_all", "best_ret", "arg_ret")}
-        st = check_scores(g, orc, rows, k, batch.dtype, r, w)
-        for kind, v in st.items():
-            x = agg.setdefault(kind, {"max_err": 0.0, "rows": 0, "exempt": 0, "exempt_index_diff": 0})
-            x["max_err"] = max(x["max_err"], v["max_err"])
-            for f in ("rows", "exempt", "exempt_index_diff"):
-                x[f] += v[f]
+        merge_scores(agg, check_scores(g, orc, rows, k, batch.dtype, r, w))
     return agg
 
 
-def check_full_problems(batch, out, problems, tau, w, n_sink, n_recent):
-    res = []
+def oracle_scores(batch, problems):
+    """The oracle's complete scores of the given (head, sequence) problems, concurrently."""
+    def one(hs):
+        h, s = hs
+        a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
+        return oracle.nn_scores(batch.keys[h, a:e], batch.dtype, batch.retained[h, a:e], batch.spec.w)
+    with ThreadPoolExecutor(ORACLE_THREADS) as ex:
+        return list(ex.map(one, problems))
+
+
+def check_full_problems(batch, out, problems, tau, n_sink, n_recent, scores=None, agg=None):
+    """Complete problems: every row of both reductions and S1 token by token."""
+    agg = {"scores": {}, "repair": {}} if agg is None else agg
+    scores = oracle_scores(batch, problems) if scores is None else scores
     s1, stt, b = host(out["s1"]), host(out["stats"]).reshape(batch.n_heads, batch.n_seqs, 4), host(out["best_ret"])
-    for (h, s) in problems:
+    res = []
+    for (h, s), sc in zip(problems, scores):
         a, e = int(batch.cu_seqlens[s]), int(batch.cu_seqlens[s + 1])
         k, r = batch.keys[h, a:e], batch.retained[h, a:e]
-        orc = oracle.repair_problem(k, batch.dtype, r, batch.budget[s], tau, w, n_sink, n_recent)
-        rows = np.arange(e - a)
+        orc = dict(sc)
+        orc.update(oracle.repair(sc["best_ret"], r, tau, n_sink, n_recent))
         g = {key: host(out[key][h, a:e]) for key in ("best_all", "arg_all", "best_ret", "arg_ret")}
-        st = check_scores(g, orc, rows, k, batch.dtype, r, w)
+        merge_scores(agg["scores"], check_scores(g, orc, np.arange(e - a), k, batch.dtype, r, batch.spec.w))
         rr = check_repair(s1[h, a:e], stt[h, s], b[h, a:e], orc, r, tau, n_sink, n_recent)
-        res.append((h, s, st, rr))
-    return res
+        merge_repairs(agg["repair"], rr)
+        res.append((h, s, rr))
+    return res, agg
 
 
-def run_repair(batch):
+def run_repair(batch, tau=None):
     sp = batch.spec
     kt, rt = to_device(batch.keys, batch.dtype), mask_to_device(batch.retained)
-    out = binding.repair(kt, rt, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent, batch.cu_seqlens)
+    out = binding.repair(kt, rt, batch.budget, sp.tau if tau is None else tau, sp.w, sp.n_sink,
+                         sp.n_recent, batch.cu_seqlens)
     import torch
     torch.cuda.synchronize()
     return out
@@ -94,47 +103,68 @@ def test_tiny_full_parity():
     batch = synth.make_batch(synth.spec("tiny"))
     sp = batch.spec
     out = run_repair(batch)
-    res = check_full_problems(batch, out, [(0, 0)], sp.tau, sp.w, sp.n_sink, sp.n_recent)
-    print("tiny", res)
-    assert res[0][3]["exact"], "tiny: S1 differs from the oracle"
+    swapped = check_all_problems(batch, out, sp.tau, sp.n_sink, sp.n_recent)
+    res, agg = check_full_problems(batch, out, [(0, 0)], sp.tau, sp.n_sink, sp.n_recent)
+    assert res[0][2]["exact"], "tiny: S1 differs from the oracle"
+    record_exemptions("tiny", {"problems_replayed": 1, "swapped": swapped, "full": agg})
 
 
+@pytest.mark.timeout(600)
 def test_llama1b_8k():
-    batch = synth.make_batch(synth.spec("llama1b_8k"))
+    batch = synth.make_batch(synth.spec("llama1b_8k"), threads=16)
     sp = batch.spec
     out = run_repair(batch)
     swapped = check_all_problems(batch, out, sp.tau, sp.n_sink, sp.n_recent)
     rng = np.random.default_rng(1)
-    agg = check_sampled_rows(batch, out, [(0, 0), (77, 0), (127, 0)], rng, sp.w)
-    res = check_full_problems(batch, out, [(5, 0), (100, 0)], sp.tau, sp.w, sp.n_sink, sp.n_recent)
-    print("llama1b_8k swapped", swapped, "sampled", agg, "full", [(r[0], r[3]) for r in res])
+    sampled = check_sampled_rows(batch, out, [(0, 0), (77, 0), (127, 0)], rng, sp.w)
+    res, agg = check_full_problems(batch, out, [(5, 0), (100, 0), (31, 0), (64, 0)], sp.tau,
+                                   sp.n_sink, sp.n_recent)
+    record_exemptions("llama1b_8k", {"problems_replayed": batch.n_heads, "swapped": swapped,
+                                     "sampled": sampled, "full": agg})
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("frac", synth.QWEN_SWEEP_BUDGETS)
 def test_qwen4b_16k_sweep(frac):
+    """One budget of the sweep at all three thresholds: every problem replayed per cell, one
+    complete problem per budget through the oracle at every threshold (b does not depend on
+    tau, so one oracle pass serves the three cells), sampled rows of two more."""
     batch = synth.make_batch(synth.spec("qwen4b_16k"), budget_frac=frac, threads=16)
     sp = batch.spec
     kt, rt = to_device(batch.keys, batch.dtype), mask_to_device(batch.retained)
+    full = [(57, 0)]
+    scores = oracle_scores(batch, full)
     rng = np.random.default_rng(2)
+    b_first = None
     for tau in synth.QWEN_SWEEP_TAUS:
         out = binding.repair(kt, rt, batch.budget, tau, sp.w, sp.n_sink, sp.n_recent, batch.cu_seqlens)
         swapped = check_all_problems(batch, out, tau, sp.n_sink, sp.n_recent)
-        if tau == synth.QWEN_SWEEP_TAUS[0]:
-            agg = check_sampled_rows(batch, out, [(3, 0), (200, 0)], rng, sp.w)
-            print("qwen4b_16k", frac, "sampled", agg)
-        print("qwen4b_16k", frac, tau, "swapped", swapped)
+        b = host(out["best_ret"])
+        if b_first is None:
+            b_first = b
+            sampled = check_sampled_rows(batch, out, [(3, 0), (200, 0)], rng, sp.w)
+        else:
+            assert np.array_equal(b, b_first), "b changed with tau"
+        res, agg = check_full_problems(batch, out, full, tau, sp.n_sink, sp.n_recent, scores=scores)
+        record_exemptions(f"qwen4b_16k budget {frac} tau {tau}",
+                          {"problems_replayed": batch.n_heads, "swapped": swapped, "full": agg,
+                           **({"sampled": sampled} if tau == synth.QWEN_SWEEP_TAUS[0] else {})})
 
 
+@pytest.mark.timeout(900)
 def test_long_aniso_32k():
     batch = synth.make_batch(synth.spec("long_aniso_32k"), threads=16)
     sp = batch.spec
     out = run_repair(batch)
     swapped = check_all_problems(batch, out, sp.tau, sp.n_sink, sp.n_recent)
     rng = np.random.default_rng(3)
-    agg = check_sampled_rows(batch, out, [(0, 0), (131, 0), (287, 0)], rng, sp.w)
-    print("long_aniso_32k swapped", swapped, "sampled", agg)
+    sampled = check_sampled_rows(batch, out, [(0, 0), (131, 0), (287, 0)], rng, sp.w)
+    res, agg = check_full_problems(batch, out, [(17, 0), (202, 0)], sp.tau, sp.n_sink, sp.n_recent)
+    record_exemptions("long_aniso_32k", {"problems_replayed": batch.n_heads, "swapped": swapped,
+                                         "sampled": sampled, "full": agg})
 
 
+@pytest.mark.timeout(900)
 def test_ragged_64x_one_launch():
     batch = synth.make_batch(synth.spec("ragged_64x"), threads=16)
     sp = batch.spec
@@ -142,6 +172,7 @@ def test_ragged_64x_one_launch():
     swapped = check_all_problems(batch, out, sp.tau, sp.n_sink, sp.n_recent)
     lens = np.diff(batch.cu_seqlens)
     shortest, longest = int(np.argmin(lens)), int(np.argmax(lens))
-    probs = [(0, shortest), (287, longest), (100, 5), (9, 40)]
-    res = check_full_problems(batch, out, probs, sp.tau, sp.w, sp.n_sink, sp.n_recent)
-    print("ragged_64x swapped", swapped, "full", [(r[0], r[1], r[3]) for r in res])
+    probs = [(0, shortest), (287, longest), (100, 5), (9, 40), (150, 63), (222, 17)]
+    res, agg = check_full_problems(batch, out, probs, sp.tau, sp.n_sink, sp.n_recent)
+    record_exemptions("ragged_64x", {"problems_replayed": batch.n_heads * batch.n_seqs,
+                                     "swapped": swapped, "full": agg})

@@ -264,20 +264,28 @@ def test_repair_budget_mismatch_and_aliasing():
                 assert s1[h, a:e].sum() == batch.budget[s]
 
 
+@pytest.mark.parametrize("want_all", [True, False], ids=["both", "retained_only"])
 @pytest.mark.parametrize("d,dtype,tau,w", [(64, "bf16", 0.9, 32), (128, "bf16", 0.85, 32),
                                            (128, "bf16", 0.95, 64), (64, "f32", 0.9, 16),
+                                           (128, "f32", 0.9, 32),
                                            (128, "bf16", 1.5, 32), (64, "bf16", -1.5, 32)])
-def test_repair_vs_oracle(d, dtype, tau, w):
+def test_repair_vs_oracle(d, dtype, tau, w, want_all):
+    """Every problem's scores, classification and S1 against the oracle; without best_all the
+    similarity sweep covers the retained columns alone (the O(nKd) form of Sec. 3.5)."""
     batch = synth.make_batch(small_spec(4, [700, 1300], d, dtype, w, 31, dup_frac=0.25))
     kt, rt = to_device(batch.keys, dtype), mask_to_device(batch.retained)
-    out = binding.repair(kt, rt, batch.budget, tau, w, 2, 3, batch.cu_seqlens)
+    out = binding.repair(kt, rt, batch.budget, tau, w, 2, 3, batch.cu_seqlens, want_all=want_all)
+    assert ("best_all" in out) == want_all
     s1, st, b = host(out["s1"]), host(out["stats"]).reshape(4, 2, 4), host(out["best_ret"])
+    gpu_all = {k: host(v) for k, v in out.items() if k.startswith(("best_", "arg_"))}
     exact = 0
     for h in range(4):
         for s in range(2):
             a, e = batch.cu_seqlens[s], batch.cu_seqlens[s + 1]
             orc = oracle.repair_problem(batch.keys[h, a:e], dtype, batch.retained[h, a:e],
                                         batch.budget[s], tau, w, 2, 3)
+            check_scores({k: v[h, a:e] for k, v in gpu_all.items()}, orc, np.arange(e - a),
+                         batch.keys[h, a:e], dtype, batch.retained[h, a:e], w)
             res = check_repair(s1[h, a:e], st[h, s], b[h, a:e], orc, batch.retained[h, a:e], tau, 2, 3)
             exact += res["exact"]
             if tau > 1 or tau < -1:
@@ -285,15 +293,27 @@ def test_repair_vs_oracle(d, dtype, tau, w):
     print("repair exact problems", exact, "of 8")
 
 
-def test_repair_skips_evicted_columns_consistently():
-    """Without best_all/arg_all the similarity kernel visits only S0 columns; b and S1 must not
-    change."""
-    batch = synth.make_batch(small_spec(9, [1500, 700], 128, "bf16", 32, 41))
-    kt, rt = to_device(batch.keys, "bf16"), mask_to_device(batch.retained)
+@pytest.mark.parametrize("d,dtype", [(64, "bf16"), (128, "bf16"), (64, "f32"), (128, "f32")])
+def test_repair_skips_evicted_columns_consistently(d, dtype):
+    """Without best_all/arg_all the similarity kernel visits only S0 columns (its own key
+    preparation copies only those): b and S1 against the oracle, and identical to the path
+    that sweeps every column."""
+    batch = synth.make_batch(small_spec(9, [1500, 700], d, dtype, 32, 41))
+    kt, rt = to_device(batch.keys, dtype), mask_to_device(batch.retained)
     full = binding.repair(kt, rt, batch.budget, 0.9, 32, 2, 3, batch.cu_seqlens, want_all=True)
     lean = binding.repair(kt, rt, batch.budget, 0.9, 32, 2, 3, batch.cu_seqlens, want_all=False)
     for k in ("s1", "stats", "best_ret", "arg_ret"):
         assert np.array_equal(host(full[k]), host(lean[k])), k
+    s1, st = host(lean["s1"]), host(lean["stats"]).reshape(9, 2, 4)
+    b, arg = host(lean["best_ret"]), host(lean["arg_ret"])
+    for h in (0, 4, 8):
+        for s in range(2):
+            a, e = batch.cu_seqlens[s], batch.cu_seqlens[s + 1]
+            k, r = batch.keys[h, a:e], batch.retained[h, a:e]
+            orc = oracle.repair_problem(k, dtype, r, batch.budget[s], 0.9, 32, 2, 3)
+            check_scores({"best_ret": b[h, a:e], "arg_ret": arg[h, a:e]}, orc, np.arange(e - a),
+                         k, dtype, r, 32)
+            check_repair(s1[h, a:e], st[h, s], b[h, a:e], orc, r, 0.9, 2, 3)
 
 
 def test_long_single_sequence_131072():
@@ -324,8 +344,9 @@ def test_long_single_sequence_131072():
                                          batch.retained[0], sp.w))
 
 
+@pytest.mark.parametrize("want_all", [True, False], ids=["both", "retained_only"])
 @pytest.mark.parametrize("seed", range(8))
-def test_random_batches_vs_oracle(seed):
+def test_random_batches_vs_oracle(seed, want_all):
     """Seeded random shapes: heads, ragged lengths (empty ones too), d, key dtype, window,
     tau, budgets and protected regions; every row of every problem against the oracle, and
     the repair through check_repair."""
@@ -347,10 +368,11 @@ def test_random_batches_vs_oracle(seed):
                     seed=seed)
     batch = synth.make_batch(sp)
     kt, rt = to_device(batch.keys, dtype), mask_to_device(batch.retained)
-    out = binding.repair(kt, rt, batch.budget, tau, w, n_sink, n_recent, batch.cu_seqlens)
+    out = binding.repair(kt, rt, batch.budget, tau, w, n_sink, n_recent, batch.cu_seqlens,
+                         want_all=want_all)
     s1, b = host(out["s1"]), host(out["best_ret"])
     st = host(out["stats"]).reshape(H, len(lens), 4)
-    gpu_all = {k: host(out[k]) for k in ("best_all", "arg_all", "best_ret", "arg_ret")}
+    gpu_all = {k: host(v) for k, v in out.items() if k.startswith(("best_", "arg_"))}
     exact = 0
     for h in range(H):
         for s in range(len(lens)):

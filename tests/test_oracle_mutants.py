@@ -61,6 +61,15 @@ MUTANTS = {
                           "score = redundancy_scores(counts, n)"),
     "evict_budget_off_by_one": ("keep[order[:min(budget, n)]] = 1", "keep[order[:min(budget + 1, n)]] = 1"),
     "prevalence_ge": ("np.sum(b > float(t))", "np.sum(b >= float(t))"),
+    # the margin band of the counts (bounds for a computation with rounded similarities)
+    "band_swapped": ('out["counts_lo"][a:a + step] = np.sum(valid & (S > tau + margin), axis=1)',
+                     'out["counts_lo"][a:a + step] = np.sum(valid & (S > tau - margin), axis=1)'),
+    "band_scaled": ('out["counts_hi"][a:a + step] = np.sum(valid & (S > tau - margin), axis=1)',
+                    'out["counts_hi"][a:a + step] = np.sum(valid & (S > tau - 10 * margin), axis=1)'),
+    "band_window_ignored": ('out["counts_hi"][a:a + step] = np.sum(valid & (S > tau - margin), axis=1)',
+                            'out["counts_hi"][a:a + step] = np.sum(S > tau - margin, axis=1)'),
+    "band_not_strict": ('out["counts_lo"][a:a + step] = np.sum(valid & (S > tau + margin), axis=1)',
+                        'out["counts_lo"][a:a + step] = np.sum(valid & (S >= tau + margin), axis=1)'),
     # Sec. 3.1 / 3.2 policy selection (reading R22)
     "select_tie_later": ("order = np.lexsort((pos, -s, nan, ~prot))",
                          "order = np.lexsort((-pos, -s, nan, ~prot))"),
