@@ -115,10 +115,23 @@ def _cut_exempt(b_o, gpu_taken, ref_taken, ranked, m, descending, tol):
     return len(diff)
 
 
+def tau_f32(tau: float) -> float:
+    """The threshold as the library receives it (a C float): the replay of the GPU's decisions
+    compares its fp32 scores with this value, so both sides decide in the kernel's precision."""
+    return float(np.float32(tau))
+
+
 def replay_repair(s1_gpu, stats_gpu, b_gpu, s0, tau, n_sink, n_recent):
     """Sec. 3.4 on the GPU's own b, by the oracle: S1 and (|O|, |D|, m) bit for bit."""
-    r = oracle.repair(np.asarray(b_gpu, dtype=np.float64), s0, tau, n_sink, n_recent)
-    assert np.array_equal(np.asarray(s1_gpu).astype(bool), r["s1"].astype(bool)), "logic replay differs"
+    t32 = tau_f32(tau)
+    r = oracle.repair(np.asarray(b_gpu, dtype=np.float64), s0, t32, n_sink, n_recent)
+    s1g = np.asarray(s1_gpu).astype(bool)
+    if not np.array_equal(s1g, r["s1"].astype(bool)):
+        d = np.flatnonzero(s1g != r["s1"].astype(bool))
+        info = [(int(i), int(np.asarray(s0)[i]), float(np.asarray(b_gpu)[i])) for i in d[:8]]
+        raise AssertionError(f"logic replay differs at {len(d)} tokens (pos, s0, b): {info}; "
+                             f"stats gpu {list(np.asarray(stats_gpu)[:3])} replay "
+                             f"{[r['n_orphan'], r['n_donor'], r['m']]}; tau32 {t32!r}")
     assert list(np.asarray(stats_gpu)[:3]) == [r["n_orphan"], r["n_donor"], r["m"]], "stats replay differs"
     return r
 
@@ -134,9 +147,10 @@ def check_repair(s1_gpu, stats_gpu, b_gpu, orc: dict, s0, tau: float, n_sink: in
     prot = oracle.protected_mask(n, n_sink, n_recent)
     assert stats_gpu[3] == 0
     replay_repair(s1g, stats_gpu, b_g, s0, tau, n_sink, n_recent)
-    # GPU classification (from its own b) against the oracle's, flag by flag
-    O_g = ~s0 & (b_g < tau)
-    D_g = s0 & ~prot & (b_g >= tau)
+    # GPU classification (from its own b, in the kernel's precision) against the oracle's
+    t32 = tau_f32(tau)
+    O_g = ~s0 & (b_g < t32)
+    D_g = s0 & ~prot & (b_g >= t32)
     O_o, D_o = orc["orphan"], orc["donor"]
     near_tau = np.abs(b_o - tau) < tol
     flips = (O_g != O_o) | (D_g != D_o)
