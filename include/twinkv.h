@@ -59,6 +59,7 @@ extern "C" {
 #define TWINKV_E_UNSUPPORTED  3  /* head dimension or dtype not supported */
 #define TWINKV_E_WORKSPACE    4  /* workspace missing or smaller than required */
 #define TWINKV_E_HIP          5  /* the HIP runtime reported an error */
+#define TWINKV_E_CAPACITY     6  /* the batch needs more than the static scratch buffer holds */
 
 /* Key element types. */
 #define TWINKV_BF16 0
@@ -156,6 +157,25 @@ int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_
                               const int64_t* budget, float tau, int n_sink, int n_recent,
                               int32_t* stats,
                               void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * twinkv_repair_from_scores for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): no workspace
+ * argument.  The only scratch the call needs, the per-sequence table, lives in a static
+ * device buffer of the library (64 KiB per GPU, held until the process ends), so at most
+ * TWINKV_NOALLOC_MAX_SEQS sequences per call; a larger batch returns TWINKV_E_CAPACITY before
+ * anything is enqueued.  The buffer of the current device is used (the stream must belong to
+ * it).  Every call on one GPU shares that buffer: calls that overlap on one GPU (different
+ * streams, or host threads enqueueing concurrently) race and must be serialised by the
+ * caller.  Nothing in the buffer needs to start at zero (each call writes the whole table it
+ * reads).  The call allocates nothing; results equal twinkv_repair_from_scores.
+ */
+#define TWINKV_NOALLOC_MAX_SEQS 2048
+int twinkv_repair_from_scores_noalloc(const float* b, const uint8_t* retained_in,
+                                      uint8_t* retained_out, int n_heads, int n_seqs,
+                                      const int64_t* cu_seqlens, const int64_t* budget,
+                                      float tau, int n_sink, int n_recent, int32_t* stats,
+                                      void* stream);
 
 /*
  * Twin counts of Sec. 3.2 Eq. 2 for every token:

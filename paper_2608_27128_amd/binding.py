@@ -25,6 +25,7 @@ OP_NN_SCORES, OP_REPAIR, OP_REPAIR_FROM_SCORES, OP_TWIN_COUNTS, OP_SCORE_EVICT, 
 MAX_TAUS = 32
 MAX_LEVELS = 4
 PROBLEM_OK, PROBLEM_BUDGET_MISMATCH, PROBLEM_NONFINITE = 0, 1, 2
+NOALLOC_MAX_SEQS = 2048
 
 _lib = None
 
@@ -42,6 +43,8 @@ SIGNATURES = {
                            _VP, _VP, _VP, _VP, _VP, _VP, _I64, _VP]),
     "twinkv_repair_from_scores": (_I, [_VP, _VP, _VP, _I, _I, _PI64, _PI64, _F, _I, _I, _VP,
                                        _VP, _I64, _VP]),
+    "twinkv_repair_from_scores_noalloc": (_I, [_VP, _VP, _VP, _I, _I, _PI64, _PI64, _F, _I, _I,
+                                               _VP, _VP]),
     "twinkv_twin_counts": (_I, [_VP, _I, _I, _I, _I, _PI64, _I64, _I64, _F, _I, _VP, _VP, _VP,
                                 _I64, _VP]),
     "twinkv_score_evict": (_I, [_VP, _I, _I, _I, _I, _PI64, _I64, _I64, _PI64, _F, _I, _I, _I,
@@ -400,6 +403,40 @@ def repair_from_scores(b, retained, budget, tau: float, n_sink: int = 4, n_recen
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_repair_from_scores", rc)
     return {"s1": s1, "stats": stats}
+
+
+def repair_from_scores_noalloc(b, retained, budget, tau: float, n_sink: int = 4,
+                               n_recent: int = 64, cu_seqlens=None, *, outputs: dict) -> dict:
+    """repair_from_scores through the entry point that allocates nothing: the caller passes
+    the output buffers (``outputs`` with "s1" uint8 (n_heads, T) and "stats" int32
+    (n_heads * n_seqs, 4)), and the library's static scratch holds the sequence table (at
+    most NOALLOC_MAX_SEQS sequences).  Calls overlapping on one GPU race."""
+    torch = _torch()
+    b = _vec2d(b, "b")
+    H, T = b.shape
+    cu = _cu(cu_seqlens, T)
+    n_seqs = len(cu) - 1
+    if retained is None:
+        raise ValueError("retained is required")
+    bud = _budget(budget, n_seqs)
+    b = _on_gpu(b, "b")
+    if not b.is_contiguous():
+        raise ValueError("b must be contiguous (the call may not allocate a copy)")
+    dev = b.device
+    if retained.dim() == 1:
+        retained = retained.unsqueeze(0)
+    if (tuple(retained.shape) != (H, T) or retained.dtype != torch.uint8 or retained.device != dev
+            or not retained.is_contiguous()):
+        raise ValueError(f"retained must be a contiguous uint8 ({H}, {T}) tensor on {dev}")
+    spec = {"s1": ((H, T), torch.uint8, dev, True), "stats": ((H * n_seqs, 4), torch.int32, dev, True)}
+    out = _check_outputs(outputs, spec, "repair_from_scores_noalloc")
+    rc = lib().twinkv_repair_from_scores_noalloc(
+        b.data_ptr(), retained.data_ptr(), out["s1"].data_ptr(), H, n_seqs, _i64_array(cu),
+        _i64_array(bud), float(tau), int(n_sink), int(n_recent), out["stats"].data_ptr(),
+        _stream(dev))
+    if rc != TWINKV_OK:
+        raise TwinKVError("twinkv_repair_from_scores_noalloc", rc)
+    return out
 
 
 def twin_counts(keys, tau: float, w: int = 32, cu_seqlens=None, *, workspace=None) -> dict:

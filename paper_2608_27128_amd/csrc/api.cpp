@@ -156,6 +156,19 @@ int max_seq_len(const int64_t* cu, int n_seqs) {
   return (int)m;
 }
 
+int check_repair_common(const uint8_t* retained_in, uint8_t* retained_out,
+                               const int64_t* budget, const int64_t* cu, int n_seqs, float tau,
+                               int n_sink, int n_recent, int32_t* stats) {
+  if (retained_in == nullptr || retained_out == nullptr || budget == nullptr || stats == nullptr)
+    return TWINKV_E_NULL;
+  if (!std::isfinite(tau)) return TWINKV_E_ARG;
+  if (n_sink < 0 || n_recent < 0) return TWINKV_E_ARG;
+  for (int s = 0; s < n_seqs; ++s) {
+    if (budget[s] < 0 || budget[s] > cu[s + 1] - cu[s]) return TWINKV_E_ARG;
+  }
+  return TWINKV_OK;
+}
+
 // Events recorded around the similarity kernel, or the compaction's gather kernel
 // (twinkv_profile_sim_events), per thread.
 thread_local hipEvent_t g_sim_start = nullptr;
@@ -275,6 +288,43 @@ int run_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_
 }
 
 }  // namespace
+
+int repair_from_scores_into(const float* b, const uint8_t* retained_in, uint8_t* retained_out,
+                            int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                            const int64_t* budget, float tau, int n_sink, int n_recent,
+                            int32_t* stats, void* table, size_t table_bytes,
+                            void* (*resolve_table)(), void* stream) {
+  if (b == nullptr) return TWINKV_E_NULL;
+  Batch bt;
+  int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
+  if (rc != TWINKV_OK) return rc;
+  rc = check_repair_common(retained_in, retained_out, budget, cu_seqlens, n_seqs, tau, n_sink,
+                           n_recent, stats);
+  if (rc != TWINKV_OK) return rc;
+  if (sizeof(SeqInfo) * (size_t)n_seqs > table_bytes) return TWINKV_E_CAPACITY;
+  if (resolve_table != nullptr && (table = resolve_table()) == nullptr) return TWINKV_E_HIP;
+  int tiles = 0;
+  std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, budget, 0, tiles);
+  SeqInfo* dtab = reinterpret_cast<SeqInfo*>(table);
+  if (launch_upload(tab.data(), sizeof(SeqInfo) * tab.size(), dtab, stream) != 0)
+    return TWINKV_E_HIP;
+  RepairArgs ra;
+  ra.b = b;
+  ra.s0 = retained_in;
+  ra.s1 = retained_out;
+  ra.seqtab = dtab;
+  ra.pmeta = nullptr;
+  ra.n_heads = n_heads;
+  ra.n_seqs = n_seqs;
+  ra.T = bt.T;
+  ra.tau = tau;
+  ra.n_sink = n_sink;
+  ra.n_recent = n_recent;
+  ra.stats = stats;
+  ra.max_len = max_seq_len(cu_seqlens, n_seqs);
+  return hip_status(launch_repair(ra, stream));
+}
+
 }  // namespace twinkv
 
 using namespace twinkv;
@@ -316,18 +366,6 @@ int twinkv_nn_scores(const void* keys, int dtype, int d, int n_heads, int n_seqs
                     /*want_all=*/true, stream, &dtab);
 }
 
-static int check_repair_common(const uint8_t* retained_in, uint8_t* retained_out,
-                               const int64_t* budget, const int64_t* cu, int n_seqs, float tau,
-                               int n_sink, int n_recent, int32_t* stats) {
-  if (retained_in == nullptr || retained_out == nullptr || budget == nullptr || stats == nullptr)
-    return TWINKV_E_NULL;
-  if (!std::isfinite(tau)) return TWINKV_E_ARG;
-  if (n_sink < 0 || n_recent < 0) return TWINKV_E_ARG;
-  for (int s = 0; s < n_seqs; ++s) {
-    if (budget[s] < 0 || budget[s] > cu[s + 1] - cu[s]) return TWINKV_E_ARG;
-  }
-  return TWINKV_OK;
-}
 
 int twinkv_repair(const void* keys, int dtype, int d, int n_heads, int n_seqs,
                   const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,
@@ -374,36 +412,15 @@ int twinkv_repair_from_scores(const float* b, const uint8_t* retained_in, uint8_
                               const int64_t* budget, float tau, int n_sink, int n_recent,
                               int32_t* stats, void* workspace, int64_t workspace_bytes,
                               void* stream) {
-  if (b == nullptr) return TWINKV_E_NULL;
   Batch bt;
   int rc = check_batch(n_heads, n_seqs, cu_seqlens, bt);
   if (rc != TWINKV_OK) return rc;
-  rc = check_repair_common(retained_in, retained_out, budget, cu_seqlens, n_seqs, tau, n_sink,
-                           n_recent, stats);
-  if (rc != TWINKV_OK) return rc;
   const Layout L = layout_for(TWINKV_OP_REPAIR_FROM_SCORES, 0, 64, bt);
   if (workspace == nullptr || workspace_bytes < (int64_t)L.total) return TWINKV_E_WORKSPACE;
-  char* ws = aligned_base(workspace);
-  int tiles = 0;
-  std::vector<SeqInfo> tab = seq_table(cu_seqlens, n_seqs, budget, 0, tiles);
-  SeqInfo* dtab = reinterpret_cast<SeqInfo*>(ws + L.seqtab);
-  if (launch_upload(tab.data(), sizeof(SeqInfo) * tab.size(), dtab, stream) != 0)
-    return TWINKV_E_HIP;
-  RepairArgs ra;
-  ra.b = b;
-  ra.s0 = retained_in;
-  ra.s1 = retained_out;
-  ra.seqtab = dtab;
-  ra.pmeta = nullptr;
-  ra.n_heads = n_heads;
-  ra.n_seqs = n_seqs;
-  ra.T = bt.T;
-  ra.tau = tau;
-  ra.n_sink = n_sink;
-  ra.n_recent = n_recent;
-  ra.stats = stats;
-  ra.max_len = max_seq_len(cu_seqlens, n_seqs);
-  return hip_status(launch_repair(ra, stream));
+  return twinkv::repair_from_scores_into(b, retained_in, retained_out, n_heads, n_seqs,
+                                         cu_seqlens, budget, tau, n_sink, n_recent, stats,
+                                         aligned_base(workspace) + L.seqtab,
+                                         L.total - kAlign, nullptr, stream);
 }
 
 int twinkv_twin_counts(const void* keys, int dtype, int d, int n_heads, int n_seqs,
@@ -713,6 +730,7 @@ const char* twinkv_status_string(int status) {
     case TWINKV_E_UNSUPPORTED: return "unsupported head dimension or key dtype";
     case TWINKV_E_WORKSPACE: return "workspace missing or too small";
     case TWINKV_E_HIP: return "HIP runtime error";
+    case TWINKV_E_CAPACITY: return "the batch needs more than the static scratch buffer holds";
     default: return "unknown status";
   }
 }

@@ -122,6 +122,16 @@ struct RepairArgs {
 // K3: orphan / donor classification, radix selection of the m most severe, swap.
 int launch_repair(const RepairArgs& a, void* stream);
 
+// The body of twinkv_repair_from_scores and of its variant without allocation: validates the
+// arguments (returning TWINKV_E_* before any HIP call), returns TWINKV_E_CAPACITY when the
+// sequence table needs more than table_bytes, then takes the table's device address from
+// resolve_table() when that is non-null (else `table`), uploads the table and launches K3.
+int repair_from_scores_into(const float* b, const uint8_t* retained_in, uint8_t* retained_out,
+                            int n_heads, int n_seqs, const int64_t* cu_seqlens,
+                            const int64_t* budget, float tau, int n_sink, int n_recent,
+                            int32_t* stats, void* table, size_t table_bytes,
+                            void* (*resolve_table)(), void* stream);
+
 struct EvictArgs {
   const int32_t* counts;     // [n_heads][T] Eq. 2 twin counts (scorer)
   const float* in_scores;    // [n_heads][T] a policy's scores (policy selection), else null

@@ -13,7 +13,7 @@ from paper_2608_27128_amd import binding
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "twinkv.h")
 
-E_NULL, E_ARG, E_UNSUP, E_WS = 1, 2, 3, 4
+E_NULL, E_ARG, E_UNSUP, E_WS, E_CAP = 1, 2, 3, 4, 6
 FAKE = 0x100000          # 16-byte aligned stand-in for a device pointer; never dereferenced
 
 
@@ -34,7 +34,7 @@ def test_exports_every_declared_function():
 
 def test_version_and_strings():
     assert binding.version() == 100
-    for code in range(6):
+    for code in range(7):
         assert binding.status_string(code) and "unknown" not in binding.status_string(code)
     assert "unknown" in binding.status_string(99)
 
@@ -130,6 +130,25 @@ def test_repair_from_scores_validation():
     assert call(tau=float("nan")) == E_ARG
     assert call(budget=(11,)) == E_ARG
     assert call(wsb=0) == E_WS
+
+
+def test_repair_from_scores_noalloc_validation():
+    """Argument and capacity errors come back before any HIP call (no GPU here): the static
+    scratch holds the table of at most 2048 sequences."""
+    L = binding.lib()
+
+    def call(b=FAKE, s0=FAKE, s1=FAKE, H=2, cu=(0, 100), bud=(50,), tau=0.9, ns=4, nr=8, st=FAKE):
+        n = len(cu) - 1
+        return L.twinkv_repair_from_scores_noalloc(b, s0, s1, H, n, cu_arr(list(cu)),
+                                                   cu_arr(list(bud)), tau, ns, nr, st, None)
+    n = binding.NOALLOC_MAX_SEQS
+    assert call(b=None) == E_NULL
+    assert call(st=None) == E_NULL
+    assert call(bud=(101,)) == E_ARG
+    assert call(tau=float("nan")) == E_ARG
+    assert call(cu=(0, 100, 90), bud=(1, 1)) == E_ARG
+    assert call(cu=tuple(range(n + 2)), bud=(1,) * (n + 1)) == E_CAP
+    assert "static scratch" in binding.status_string(E_CAP)
 
 
 def test_twin_counts_validation():
