@@ -37,37 +37,75 @@ __device__ inline int sel_exclusive_scan(int v, int* s_wave, int& total) {
   return base + x - v;
 }
 
+// One histogram increment per lane with mem set.  The lanes that share the bin of the first
+// such lane add through that lane alone (keys are often concentrated in a few bins, where
+// plain LDS atomics from one instruction would serialise on one address); the others add
+// their own.  All lanes of the wave must call it.
+__device__ inline void hist_add(bool mem, int bin, int* s_hist) {
+  const uint64_t act = __ballot(mem);
+  if (act == 0ull) return;
+  const int leader = __ffsll((long long)act) - 1;
+  const int lbin = __builtin_amdgcn_readlane(bin, leader);
+  const bool peer = mem && bin == lbin;
+  const uint64_t peers = __ballot(peer);
+  if ((int)(threadIdx.x & 63) == leader) atomicAdd(&s_hist[lbin], (int)__popcll(peers));
+  if (mem && !peer) atomicAdd(&s_hist[bin], 1);
+}
+
 // Among the members of [0, len) (member(t, key) returns true and sets key), the rank-th
 // smallest key (1-based rank, 1 <= rank <= number of members).  Returns that key; take_eq
 // receives how many members equal to it are needed so that exactly `rank` are taken when
-// every member below it is taken.  Workspace: s_hist[kSelBins], s_wave[NT / 64], s_pick[2].
-// Every thread of the block must call it.
-template <int NT, class Member>
+// every member below it is taken, and eq_total (if non-null) how many members equal it.
+// Workspace: s_hist[kSelBins], s_wave[NT / 64], s_pick[3].  Every thread of the block must
+// call it.
+// Digits: BITS = 11 gives three passes of 11/11/10 bits over 2048 bins; BITS = 8 gives four
+// passes of 8 bits over 256 bins (cheaper clears and scans for short sequences).
+template <int BITS>
+struct SelDigits;
+template <>
+struct SelDigits<11> {
+  static constexpr int PASSES = 3, BINS = 2048;
+  static __device__ constexpr int shift(int p) { return p == 0 ? 21 : (p == 1 ? 10 : 0); }
+  static __device__ constexpr int width(int p) { return p == 2 ? 10 : 11; }
+};
+template <>
+struct SelDigits<8> {
+  static constexpr int PASSES = 4, BINS = 256;
+  static __device__ constexpr int shift(int p) { return 24 - 8 * p; }
+  static __device__ constexpr int width(int) { return 8; }
+};
+
+template <int NT, class Member, int BITS = 11>
 __device__ inline uint32_t block_select(int len, int rank, Member member, int* s_hist,
-                                        int* s_wave, int* s_pick, int& take_eq) {
+                                        int* s_wave, int* s_pick, int& take_eq,
+                                        int* eq_total = nullptr) {
+  using Dg = SelDigits<BITS>;
+  static_assert(Dg::BINS % NT == 0 || NT % Dg::BINS == 0, "bins and threads must tile");
   const int tid = threadIdx.x;
   uint32_t prefix = 0u, mask = 0u;
   int kk = rank;
-  const int shifts[3] = {21, 10, 0};
-  const int widths[3] = {11, 11, 10};
 #pragma unroll
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = shifts[pass];
-    const uint32_t dmask = (1u << widths[pass]) - 1u;
-    for (int b = tid; b < kSelBins; b += NT) s_hist[b] = 0;
+  for (int pass = 0; pass < Dg::PASSES; ++pass) {
+    const int shift = Dg::shift(pass);
+    const uint32_t dmask = (1u << Dg::width(pass)) - 1u;
+    for (int b = tid; b < Dg::BINS; b += NT) s_hist[b] = 0;
     __syncthreads();
-    for (int t = tid; t < len; t += NT) {
-      uint32_t key;
-      if (member(t, key) && (key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & dmask], 1);
+    // uniform trip count over the block, so that every lane of a wave takes part in the
+    // ballots of hist_add
+    for (int t0 = 0; t0 < len; t0 += NT) {
+      const int t = t0 + tid;
+      uint32_t key = 0u;
+      const bool mem = t < len && member(t, key) && (key & mask) == prefix;
+      hist_add(mem, (int)((key >> shift) & dmask), s_hist);
     }
     __syncthreads();
-    // thread tid owns the BPT consecutive bins from BPT * tid
-    constexpr int BPT = kSelBins / NT;
+    // thread tid owns the BPT consecutive bins from BPT * tid (none past the last bin)
+    constexpr int BPT = Dg::BINS >= NT ? Dg::BINS / NT : 1;
     int hs[BPT];
     int sum = 0;
 #pragma unroll
     for (int k = 0; k < BPT; ++k) {
-      hs[k] = s_hist[BPT * tid + k];
+      hs[k] = BPT * tid + k < Dg::BINS ? s_hist[BPT * tid + k] : 0;
       sum += hs[k];
     }
     int dummy;
@@ -77,6 +115,7 @@ __device__ inline uint32_t block_select(int len, int rank, Member member, int* s
       if (before < kk && kk <= before + hs[k]) {
         s_pick[0] = BPT * tid + k;
         s_pick[1] = before;
+        s_pick[2] = hs[k];
       }
       before += hs[k];
     }
@@ -84,6 +123,7 @@ __device__ inline uint32_t block_select(int len, int rank, Member member, int* s
     kk -= s_pick[1];
     prefix |= (uint32_t)s_pick[0] << shift;
     mask |= dmask << shift;
+    if (pass == Dg::PASSES - 1 && eq_total != nullptr) *eq_total = s_pick[2];
     __syncthreads();
   }
   take_eq = kk;

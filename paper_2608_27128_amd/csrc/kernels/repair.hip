@@ -6,16 +6,25 @@
 //   highest b (ties: lowest position first); S1 has exactly |S0| members.
 //
 // Since m = min(|O|, |D|), at least one side is taken whole; the other side needs the
-// m-th smallest key, found by an MSB-first radix select (11/11/10-bit digits, LDS
-// histograms) on order-preserving float keys, then a pass in position order that takes exactly
-// the remaining members equal to that key (ranked by wave ballots, slab by slab).  1024
-// threads per problem (256 when every sequence is short).  For sequences of up to 32768
+// m-th smallest key, found by an MSB-first radix select on order-preserving float keys
+// (11/11/10-bit digits over 2048 LDS bins with 1024 threads per problem; 8-bit digits over
+// 256 bins with 256 threads when every sequence has at most 4096 tokens), then a pass in
+// position order that takes exactly the remaining members equal to that key (ranked by wave
+// ballots, slab by slab) when some of them must be left out.  For sequences of up to 32768
 // tokens, b and S0 are read from HBM once (5 bytes per token) into LDS and every later pass
 // reads LDS; longer ones stream them from global memory on every pass.
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"
 #include "block_select.h"
+
+// Build-time variants of the short-sequence path (tuning sweeps).
+#ifndef TWINKV_K3_SHORT_THREADS
+#define TWINKV_K3_SHORT_THREADS 256
+#endif
+#ifndef TWINKV_K3_SHORT_BITS
+#define TWINKV_K3_SHORT_BITS 8
+#endif
 
 namespace twinkv {
 namespace {
@@ -29,15 +38,26 @@ __device__ inline uint32_t ord_key(float x) {
 // CAP > 0: the problem's b and S0 (as a bit array) are copied to LDS in the first pass, so
 // HBM is read once and the selection passes run from LDS (sequences of at most CAP tokens).
 // CAP = 0: every pass reads global memory.
-template <int NT, int CAP>
+//
+// Latency: the count pass and the final pass take U tokens per thread per round, with all of
+// a round's loads issued before any is used; the counts are summed per wave from ballots and
+// reduced across the block once; the position-ordered ranking of members equal to the cut
+// key (two barriers per slab) only runs when some of them must be left out.
+template <int NT, int CAP, int BITS>
 __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
   static_assert(CAP % NT == 0 && CAP % 64 == 0, "the cache holds whole slabs");
-  __shared__ int s_wave[NT / 64];
-  __shared__ int s_hist[kSelBins];
-  __shared__ int s_pick[2];
+  constexpr int U = 8;
+  constexpr int NW = NT / 64;
+  __shared__ int s_wave[NW];
+  __shared__ int s_red[4][NW];
+  __shared__ int s_hist[SelDigits<BITS>::BINS];
+  __shared__ int s_pick[3];
   __shared__ float s_b[CAP > 0 ? CAP : 1];
   __shared__ uint32_t s_r[CAP > 0 ? CAP / 32 : 1];
 
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int q = blockIdx.x;
   const int h = q / a.n_seqs;
   const int s = q - h * a.n_seqs;
@@ -49,9 +69,6 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
   uint8_t* s1 = a.s1 + base;
   const float tau = a.tau;
   const int rec0 = len - a.n_recent;  // first recent-window position
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
   auto is_orphan = [&](int t, float x, bool r) { return !r && x < tau; };
   auto is_donor = [&](int t, float x, bool r) {
     return r && !(t < a.n_sink || t >= rec0) && x >= tau;
@@ -65,34 +82,54 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
     else return s0[t] != 0;
   };
 
-  // ---- pass 1: counts (and the LDS copy), in slabs of NT consecutive tokens ----
+  // ---- pass 1: counts (and the LDS copy), U slabs of NT tokens per round ----
+  // per-wave counts from ballots (wave-uniform scalars)
   int c_ret = 0, c_o = 0, c_d = 0, bad = 0;
-  for (int t0 = 0; t0 < len; t0 += NT) {
-    const int t = t0 + tid;
-    const bool valid = t < len;
-    const float x = valid ? b[t] : 0.0f;
-    const bool r = valid && s0[t] != 0;
-    if constexpr (CAP > 0) {
-      if (valid) s_b[t] = x;
-      const uint64_t bal = __ballot(r);
-      if (lane == 0) {
-        const int w0 = (t0 + 64 * wave) >> 5;
-        s_r[w0] = (uint32_t)bal;
-        s_r[w0 + 1] = (uint32_t)(bal >> 32);
-      }
+  for (int t0 = 0; t0 < len; t0 += U * NT) {
+    float x[U];
+    bool r[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = t0 + u * NT + tid;
+      x[u] = t < len ? b[t] : 0.0f;
+      r[u] = t < len && s0[t] != 0;
     }
-    if (valid) {
-      bad |= !(fabsf(x) <= 3.4e38f);
-      c_ret += r;
-      c_o += is_orphan(t, x, r);
-      c_d += is_donor(t, x, r);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int slab = t0 + u * NT;
+      if (slab >= len) break;  // uniform over the block
+      const int t = slab + tid;
+      const bool valid = t < len;
+      const uint64_t rb = __ballot(r[u]);
+      if constexpr (CAP > 0) {
+        if (valid) s_b[t] = x[u];
+        if (lane == 0) {
+          const int w0 = (slab + 64 * wave) >> 5;
+          s_r[w0] = (uint32_t)rb;
+          s_r[w0 + 1] = (uint32_t)(rb >> 32);
+        }
+      }
+      c_ret += (int)__popcll(rb);
+      c_o += (int)__popcll(__ballot(valid && is_orphan(t, x[u], r[u])));
+      c_d += (int)__popcll(__ballot(valid && is_donor(t, x[u], r[u])));
+      bad |= (int)(__ballot(valid && !(fabsf(x[u]) <= 3.4e38f)) != 0ull);
     }
   }
-  int tot_ret, tot_o, tot_d, tot_bad;
-  (void)sel_exclusive_scan<NT>(c_ret, s_wave, tot_ret);
-  (void)sel_exclusive_scan<NT>(c_o, s_wave, tot_o);
-  (void)sel_exclusive_scan<NT>(c_d, s_wave, tot_d);
-  (void)sel_exclusive_scan<NT>(bad, s_wave, tot_bad);  // its barriers also publish the copy
+  if (lane == 0) {
+    s_red[0][wave] = c_ret;
+    s_red[1][wave] = c_o;
+    s_red[2][wave] = c_d;
+    s_red[3][wave] = bad;
+  }
+  __syncthreads();  // also publishes the LDS copy
+  int tot_ret = 0, tot_o = 0, tot_d = 0, tot_bad = 0;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) {
+    tot_ret += s_red[0][k];
+    tot_o += s_red[1][k];
+    tot_d += s_red[2][k];
+    tot_bad |= s_red[3][k];
+  }
 
   int status = 0;
   if (tot_bad || (a.pmeta && (a.pmeta[q].flags & kFlagNonfinite))) status = 2;
@@ -103,57 +140,36 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
 
   // ---- radix select of the m-th smallest key on the side that is cut ----
   uint32_t key_cut = 0xFFFFFFFFu;
-  int take_eq = 0;
+  int take_eq = 0, eq_total = 0;
   if (sel_o || sel_d) {
-    key_cut = block_select<NT>(
-        len, m,
-        [&](int t, uint32_t& key) {
-          const float x = bval(t);
-          const bool r = rbit(t);
-          if (sel_o) {
-            key = ord_key(x);
-            return is_orphan(t, x, r);
-          }
-          key = ~ord_key(x);
-          return is_donor(t, x, r);
-        },
-        s_hist, s_wave, s_pick, take_eq);
+    auto member = [&](int t, uint32_t& key) {
+      const float x = bval(t);
+      const bool r = rbit(t);
+      if (sel_o) {
+        key = ord_key(x);
+        return is_orphan(t, x, r);
+      }
+      key = ~ord_key(x);
+      return is_donor(t, x, r);
+    };
+    key_cut = block_select<NT, decltype(member), BITS>(len, m, member, s_hist, s_wave, s_pick,
+                                                       take_eq, &eq_total);
   }
+  // every member equal to the cut key is taken unless some must be left out
+  const bool rank_eq = (sel_o || sel_d) && take_eq < eq_total;
 
-  // ---- final pass, slab by slab: members equal to the cut key are ranked by position ----
-  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
-  int eq_before = 0;
-  for (int t0 = 0; t0 < len; t0 += NT) {
-    const int t = t0 + tid;
-    const bool valid = t < len;
-    const float x = valid ? bval(t) : 0.0f;
-    const bool r = valid && rbit(t);
-    const bool orphan = valid && is_orphan(t, x, r);
-    const bool donor = valid && is_donor(t, x, r);
-    bool eq = false;
-    if (sel_o) eq = orphan && ord_key(x) == key_cut;
-    else if (sel_d) eq = donor && ~ord_key(x) == key_cut;
-    const uint64_t bal = __ballot(eq);
-    if (lane == 0) s_wave[wave] = __popcll(bal);
-    __syncthreads();
-    int rank = eq_before + __popcll(bal & below);
-#pragma unroll
-    for (int k = 0; k < NT / 64; ++k) {
-      const int c = s_wave[k];
-      rank += k < wave ? c : 0;
-      eq_before += c;
-    }
-    __syncthreads();
+  // the decision for one token, given the rank of an equal-to-cut member among its peers
+  auto decide = [&](int t, float x, bool r, int rank) -> uint8_t {
     uint8_t out = r ? 1 : 0;
     if (m > 0) {
-      if (orphan) {
+      if (is_orphan(t, x, r)) {
         bool admit = true;
         if (sel_o) {
           const uint32_t key = ord_key(x);
           admit = key < key_cut || (key == key_cut && rank < take_eq);
         }
         if (admit) out = 1;
-      } else if (donor) {
+      } else if (is_donor(t, x, r)) {
         bool evict = true;
         if (sel_d) {
           const uint32_t key = ~ord_key(x);
@@ -162,7 +178,53 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
         if (evict) out = 0;
       }
     }
-    if (valid) s1[t] = out;
+    return out;
+  };
+
+  if (!rank_eq) {
+    // ---- final pass without ranking: U tokens per thread per round, no barriers ----
+    for (int t0 = 0; t0 < len; t0 += U * NT) {
+      float x[U];
+      bool r[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int t = t0 + u * NT + tid;
+        x[u] = t < len ? bval(t) : 0.0f;
+        r[u] = t < len && rbit(t);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int t = t0 + u * NT + tid;
+        if (t < len) s1[t] = decide(t, x[u], r[u], 0);
+      }
+    }
+  } else {
+    // ---- final pass, slab by slab: members equal to the cut key are ranked by position ----
+    const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+    int eq_before = 0;
+    for (int t0 = 0; t0 < len; t0 += NT) {
+      const int t = t0 + tid;
+      const bool valid = t < len;
+      const float x = valid ? bval(t) : 0.0f;
+      const bool r = valid && rbit(t);
+      bool eq = false;
+      if (valid) {
+        if (sel_o) eq = is_orphan(t, x, r) && ord_key(x) == key_cut;
+        else eq = is_donor(t, x, r) && ~ord_key(x) == key_cut;
+      }
+      const uint64_t bal = __ballot(eq);
+      if (lane == 0) s_wave[wave] = __popcll(bal);
+      __syncthreads();
+      int rank = eq_before + __popcll(bal & below);
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        const int c = s_wave[k];
+        rank += k < wave ? c : 0;
+        eq_before += c;
+      }
+      __syncthreads();
+      if (valid) s1[t] = decide(t, x, r, rank);
+    }
   }
   if (tid == 0) {
     int32_t* st = a.stats + 4 * (int64_t)q;
@@ -180,16 +242,17 @@ int launch_repair(const RepairArgs& a, void* stream) {
   if (P == 0) return hipSuccess;
   hipStream_t st = (hipStream_t)stream;
   const dim3 grid((unsigned)P);
-  // the smallest LDS copy that holds the longest sequence; short sequences use 256 threads
-  // so that more problems are in flight
+  // the smallest LDS copy that holds the longest sequence; short sequences with fewer
+  // threads and 8-bit digits
   if (a.max_len <= 4096)
-    hipLaunchKernelGGL((repair_kernel<256, 4096>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<TWINKV_K3_SHORT_THREADS, 4096, TWINKV_K3_SHORT_BITS>), grid,
+                       dim3(TWINKV_K3_SHORT_THREADS), 0, st, a);
   else if (a.max_len <= 16384)
-    hipLaunchKernelGGL((repair_kernel<1024, 16384>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<1024, 16384, 11>), grid, dim3(1024), 0, st, a);
   else if (a.max_len <= 32768)
-    hipLaunchKernelGGL((repair_kernel<1024, 32768>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<1024, 32768, 11>), grid, dim3(1024), 0, st, a);
   else
-    hipLaunchKernelGGL((repair_kernel<1024, 0>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<1024, 0, 11>), grid, dim3(1024), 0, st, a);
   return hipGetLastError();
 }
 

@@ -44,7 +44,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
   static_assert(CAP % NT == 0, "the cache holds whole slabs");
   __shared__ int s_wave[NT / 64];
   __shared__ int s_hist[kSelBins];
-  __shared__ int s_pick[2];
+  __shared__ int s_pick[3];
   __shared__ int s_nan;
   __shared__ uint32_t s_c[CAP > 0 ? CAP : 1];
 
