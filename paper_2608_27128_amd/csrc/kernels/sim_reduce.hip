@@ -51,10 +51,17 @@ template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC, int FG>
 struct Cfg {
   static_assert(FG == 1 || FG == CPT, "results merge per chunk or per tile");
   static constexpr int WG_PER_CU = OCC * 4 / NWAVES;  // OCC waves per SIMD
+  // count mode's epilogue holds more registers: at most 2 waves per SIMD
+  static constexpr int WG_PER_CU_COUNT = (OCC < 2 ? OCC : 2) * 4 / NWAVES;
   static constexpr int KSTEPS = SPLIT ? 3 * D / 16 : D / 16;
   static constexpr int DCOL = SPLIT ? 2 * D : D;      // bf16 elements per column in LDS
   static constexpr int PPC = DCOL / 8;                // 16-byte pieces per column
   static constexpr int SWZ = (PPC < 16 ? PPC : 16) - 1;  // piece-index XOR swizzle mask
+  // columns sharing one 256-byte LDS bank row (2 at d = 64 bf16), and the period in
+  // columns of the swizzle ((column / CPR) & SWZ)
+  static constexpr int CPR = DCOL * 2 < 256 ? 256 / (DCOL * 2) : 1;
+  static constexpr int SWZ_PERIOD = (SWZ + 1) * CPR;
+  static_assert(kChunk % SWZ_PERIOD == 0, "a chunk's columns repeat the swizzle");
   static constexpr int TN = CPT * kChunk;             // columns per LDS tile
   static constexpr int NT = NWAVES * 64;
   static constexpr int RB = NWAVES * NSUB * 32;       // rows per workgroup
@@ -201,7 +208,10 @@ __device__ inline void to_chunk_form(uint32_t& run, int& cid) {
 }
 
 template <int D, bool SPLIT, int NSUB, int NWAVES, int CPT, int OCC, int FG, bool COUNT>
-__global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kernel(SimArgs a) {
+__global__ __launch_bounds__(NWAVES * 64,
+                             (COUNT ? Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC, FG>::WG_PER_CU_COUNT
+                                    : Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC, FG>::WG_PER_CU))
+void sim_reduce_kernel(SimArgs a) {
   using C = Cfg<D, SPLIT, NSUB, NWAVES, CPT, OCC, FG>;
   constexpr uint32_t LOW = Slots<FG>::LOW;
   static_assert(kGroupAlign % C::TN == 0, "the evicted group must start on a tile boundary");
@@ -398,15 +408,18 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   };
 
   // ---- LDS addressing ------------------------------------------------------------------
-  // A column's 16-byte piece p is stored in slot p ^ (column & SWZ) of its row, so the 32
-  // lanes that read one piece of 32 consecutive columns hit distinct banks.  Since SWZ < 32,
-  // the swizzle of column c*32 + l32 only depends on l32: the byte offset of k-step t of a
-  // lane's column is a lane constant plus c * (chunk bytes) plus the stage offset.
+  // A column's 16-byte piece p is stored in slot p ^ ((column / CPR) & SWZ) of its row, so
+  // the lanes that read one piece of consecutive columns in one LDS pass hit distinct banks
+  // (with two 128-byte columns per 256-byte bank row at d = 64, the even and the odd columns
+  // take the two halves of the row and the swizzle changes every second column).  The
+  // swizzle repeats every SWZ_PERIOD columns, which divides 32, so for column c*32 + l32 it
+  // only depends on l32: the byte offset of k-step t of a lane's column is a lane constant
+  // plus c * (chunk bytes) plus the stage offset.
   int aoff[C::KSTEPS];
 #pragma unroll
   for (int t = 0; t < C::KSTEPS; ++t) {
     const int part = (col_off<D, SPLIT>(t) >> 3) + half;
-    aoff[t] = l32 * (C::DCOL * 2) + ((part ^ (l32 & C::SWZ)) << 4);
+    aoff[t] = l32 * (C::DCOL * 2) + ((part ^ ((l32 / C::CPR) & C::SWZ)) << 4);
   }
   const int roff = C::KEY_BYTES + 16 * half;  // this lane's inverse norms inside a chunk
 
@@ -424,17 +437,18 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
   // ---- column tiles: global -> LDS by direct (asynchronous) loads, double buffered ------
   // Each wave moves LOADS_PER_WAVE blocks of 1 KB with buffer loads; lane l of a block lands
   // at byte 16*l.  Block blk holds columns blk*B .. blk*B+B-1 (B = 64 / PPC), lane l piece
-  // l % PPC of column blk*B + l / PPC, stored in slot piece ^ (column & SWZ).  The buffer
-  // resource of a tile ends at the problem's last column, so the hardware range check turns
-  // loads past it into zeros instead of reads (those columns are never used).
+  // l % PPC of column blk*B + l / PPC, stored in slot piece ^ ((column / CPR) & SWZ).  The
+  // buffer resource of a tile ends at the problem's last column, so the hardware range check
+  // turns loads past it into zeros instead of reads (those columns are never used).
   constexpr int B = 64 / C::PPC;
-  static_assert((C::SWZ + 1) % B == 0 && ((C::LOADS_PER_WAVE * B) % (C::SWZ + 1)) == 0,
+  constexpr int NV = C::SWZ_PERIOD / B;  // distinct lane offsets over a wave's blocks
+  static_assert(C::SWZ_PERIOD % B == 0 && ((C::LOADS_PER_WAVE * B) % C::SWZ_PERIOD) == 0,
                 "the swizzle of a block's columns must repeat with the block index");
   const int lcol = lane / C::PPC;
-  int vlane[(C::SWZ + 1) / B];
+  int vlane[NV];
 #pragma unroll
-  for (int r = 0; r < (C::SWZ + 1) / B; ++r)
-    vlane[r] = lcol * (C::DCOL * 2) + 16 * ((lane % C::PPC) ^ (r * B + lcol));
+  for (int r = 0; r < NV; ++r)
+    vlane[r] = lcol * (C::DCOL * 2) + 16 * ((lane % C::PPC) ^ (((r * B + lcol) / C::CPR) & C::SWZ));
   auto issue_tile = [&](int tile, int buf) {
     char* st = smem + buf * C::STAGE;
     const int64_t first = (int64_t)tile * C::TN;
@@ -447,7 +461,7 @@ __global__ __launch_bounds__(NWAVES * 64, OCC * 4 / NWAVES) void sim_reduce_kern
       const int blk = wave * C::LOADS_PER_WAVE + kk;
       const int rem = nbytes - blk * 1024;
       load_block_lds16(pk + (first * C::DCOL + blk * 512), rem > 0 ? rem : 0,
-                       vlane[kk % ((C::SWZ + 1) / B)], st + blk * 1024);
+                       vlane[kk % NV], st + blk * 1024);
     }
     // The column tables (inverse norms, then positions) in 256-byte pieces, 4 bytes a lane.
     const int tbytes = (left < C::TN ? left : C::TN) * 4;
@@ -761,7 +775,7 @@ hipError_t run(const SimArgs& a, hipStream_t st) {
 #define TWINKV_CFG_BF16_128 128, false, 3, 4, 4, 2, 4
 #endif
 #ifndef TWINKV_CFG_BF16_64
-#define TWINKV_CFG_BF16_64 64, false, 4, 4, 2, 2, 1
+#define TWINKV_CFG_BF16_64 64, false, 4, 4, 2, 3, 1
 #endif
 #ifndef TWINKV_CFG_F32_64
 #define TWINKV_CFG_F32_64 64, true, 1, 4, 4, 2, 1
