@@ -4,7 +4,9 @@
 
 Kernels (csrc/kernels/*.hip) are compiled by hipcc for gfx950 with packed-fp32 VALU
 instructions disabled; the host layer (csrc/api.cpp) is plain C++ against the HIP
-runtime API.  Everything is linked into paper_2608_27128_amd/libtwinkv.so.
+runtime API.  Everything is linked into paper_2608_27128_amd/libtwinkv.so.  A second copy
+built with -DTWINKV_DEBUG (kernels that poison their LDS between uses, with extra barriers)
+goes to paper_2608_27128_amd/libtwinkv_debug.so; only the tests load it.
 """
 from __future__ import annotations
 
@@ -51,26 +53,36 @@ def _run(cmd, verbose):
         print("\n".join(noise), file=sys.stderr)
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libtwinkv.so; returns the library path."""
+DEBUG_LIB = os.path.join(HERE, "libtwinkv_debug.so")
+
+
+def _build_one(lib: str, objdir: str, extra: list, verbose: bool) -> str:
     hipcc = os.path.join(ROCM, "bin", "hipcc")
     cxx = shutil.which("g++") or "g++"
-    os.makedirs(BUILD, exist_ok=True)
+    os.makedirs(objdir, exist_ok=True)
     jobs = []
     objs = []
     for src in sorted(glob.glob(os.path.join(CSRC, "kernels", "*.hip"))):
-        obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-        jobs.append([hipcc, *HIP_FLAGS, "-c", src, "-o", obj])
+        obj = os.path.join(objdir, os.path.basename(src) + ".o")
+        jobs.append([hipcc, *HIP_FLAGS, *extra, "-c", src, "-o", obj])
         objs.append(obj)
-    api_obj = os.path.join(BUILD, "api.cpp.o")
+    api_obj = os.path.join(objdir, "api.cpp.o")
     jobs.append([cxx, *CXX_FLAGS, "-c", os.path.join(CSRC, "api.cpp"), "-o", api_obj])
     objs.append(api_obj)
     with ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         list(ex.map(lambda c: _run(c, verbose), jobs))
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     _run([hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp,
           f"-L{os.path.join(ROCM, 'lib')}", "-lamdhip64"], verbose)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source and link libtwinkv.so, plus libtwinkv_debug.so (the LDS-poisoning
+    build the tests compare against it, -DTWINKV_DEBUG); returns the library path."""
+    _build_one(LIB, BUILD, [], verbose)
+    _build_one(DEBUG_LIB, os.path.join(BUILD, "debug"), ["-DTWINKV_DEBUG"], verbose)
     return LIB
 
 

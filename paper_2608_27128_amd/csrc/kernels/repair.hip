@@ -82,6 +82,16 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
     else return s0[t] != 0;
   };
 
+#ifdef TWINKV_DEBUG
+  // Debug build: the LDS copy and the histogram start as poison (NaN scores, all S0 bits set),
+  // so a read of a slot the count pass did not fill changes the result.
+  if constexpr (CAP > 0) {
+    for (int i = tid; i < CAP; i += NT) s_b[i] = __uint_as_float(~0u);
+    for (int i = tid; i < CAP / 32; i += NT) s_r[i] = ~0u;
+  }
+  for (int i = tid; i < SelDigits<BITS>::BINS; i += NT) s_hist[i] = -1;
+  __syncthreads();
+#endif
   // ---- pass 1: counts (and the LDS copy), U slabs of NT tokens per round ----
   // per-wave counts from ballots (wave-uniform scalars)
   int c_ret = 0, c_o = 0, c_d = 0, bad = 0;

@@ -578,6 +578,15 @@ void sim_reduce_kernel(SimArgs a) {
   // sequence) only takes its share of the tile loads; its SIMD's MFMA pipe is left to the
   // other workgroup's wave.
   const bool active = wrow0 < len;
+#ifdef TWINKV_DEBUG
+  // Debug build: both stages and the parked results start as poison.
+  {
+    uint4* all = reinterpret_cast<uint4*>(smem);
+    for (int i = threadIdx.x; i < (2 * C::STAGE + C::RETIRED) / 16; i += C::NT)
+      all[i] = make_uint4(~0u, ~0u, ~0u, ~0u);
+  }
+  __syncthreads();
+#endif
   if (ntiles > 0) issue_tile(0, 0);
 #pragma unroll 1
   for (int tile = 0; tile < ntiles; ++tile) {
@@ -602,6 +611,19 @@ void sim_reduce_kernel(SimArgs a) {
       if (buf == 0) sweep_tile(std::integral_constant<int, 0>{}, c0, keep);
       else sweep_tile(std::integral_constant<int, 1>{}, c0, keep);
     }
+#ifdef TWINKV_DEBUG
+    // Debug build: once every wave has swept this stage, fill it with 0xFF bytes (NaN keys
+    // and inverse norms, position -1) before the next tile's loads refill it.  A read of a
+    // stage outside its tile's lifetime then sees the poison, and the results differ from
+    // the normal build's.
+    __syncthreads();
+    {
+      uint4* stg = reinterpret_cast<uint4*>(smem + buf * C::STAGE);
+      for (int i = threadIdx.x; i < C::STAGE / 16; i += C::NT)
+        stg[i] = make_uint4(~0u, ~0u, ~0u, ~0u);
+    }
+    __syncthreads();
+#endif
   }
   reduce_into(pacc, prv, pgc, CPT - 1, NSUB - 1, pmask);
   flush(NSUB - 1, (ntiles - 1) * CPT);
