@@ -58,28 +58,18 @@ __device__ inline void hist_add(bool mem, int bin, int* s_hist) {
 // every member below it is taken, and eq_total (if non-null) how many members equal it.
 // Workspace: s_hist[kSelBins], s_wave[NT / 64], s_pick[3].  Every thread of the block must
 // call it.
-// Digits: BITS = 11 gives three passes of 11/11/10 bits over 2048 bins; BITS = 8 gives four
-// passes of 8 bits over 256 bins (cheaper clears and scans for short sequences).
-template <int BITS>
-struct SelDigits;
-template <>
-struct SelDigits<11> {
-  static constexpr int PASSES = 3, BINS = 2048;
+// Digits: three passes of 11/11/10 bits over kSelBins = 2048 bins.
+struct SelDigits {
+  static constexpr int PASSES = 3, BINS = kSelBins;
   static __device__ constexpr int shift(int p) { return p == 0 ? 21 : (p == 1 ? 10 : 0); }
   static __device__ constexpr int width(int p) { return p == 2 ? 10 : 11; }
 };
-template <>
-struct SelDigits<8> {
-  static constexpr int PASSES = 4, BINS = 256;
-  static __device__ constexpr int shift(int p) { return 24 - 8 * p; }
-  static __device__ constexpr int width(int) { return 8; }
-};
 
-template <int NT, class Member, int BITS = 11>
+template <int NT, class Member>
 __device__ inline uint32_t block_select(int len, int rank, Member member, int* s_hist,
                                         int* s_wave, int* s_pick, int& take_eq,
                                         int* eq_total = nullptr) {
-  using Dg = SelDigits<BITS>;
+  using Dg = SelDigits;
   static_assert(Dg::BINS % NT == 0 || NT % Dg::BINS == 0, "bins and threads must tile");
   const int tid = threadIdx.x;
   uint32_t prefix = 0u, mask = 0u;

@@ -6,24 +6,24 @@
 //   highest b (ties: lowest position first); S1 has exactly |S0| members.
 //
 // Since m = min(|O|, |D|), at least one side is taken whole; the other side needs the
-// m-th smallest key, found by an MSB-first radix select on order-preserving float keys
-// (11/11/10-bit digits over 2048 LDS bins with 1024 threads per problem; 8-bit digits over
-// 256 bins with 256 threads when every sequence has at most 4096 tokens), then a pass in
-// position order that takes exactly the remaining members equal to that key (ranked by wave
-// ballots, slab by slab) when some of them must be left out.  For sequences of up to 32768
-// tokens, b and S0 are read from HBM once (5 bytes per token) into LDS and every later pass
-// reads LDS; longer ones stream them from global memory on every pass.
+// m-th smallest key, found by an MSB-first radix select on order-preserving float keys, then
+// a pass in position order that takes exactly the remaining members equal to that key
+// (ranked by wave ballots) when some of them must be left out.
+//  * Up to 4096 tokens per sequence (repair_short_kernel, 256 threads): the tokens stay in
+//    registers, the cut side's keys are compacted into LDS and selected with four 8-bit
+//    digit passes.
+//  * Longer sequences (repair_kernel, 1024 threads): 11/11/10-bit digits over 2048 LDS bins;
+//    up to 32768 tokens, b and S0 are read from HBM once (5 bytes per token) into LDS and
+//    every later pass reads LDS; longer ones stream them from global memory on every pass.
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"
 #include "block_select.h"
 
-// Build-time variants of the short-sequence path (tuning sweeps).
+// Threads per problem of the short-sequence path (build-time tuning; 256 measured best
+// against 128 and 512 on 1k-4k-token sequences).
 #ifndef TWINKV_K3_SHORT_THREADS
 #define TWINKV_K3_SHORT_THREADS 256
-#endif
-#ifndef TWINKV_K3_SHORT_BITS
-#define TWINKV_K3_SHORT_BITS 8
 #endif
 
 namespace twinkv {
@@ -43,14 +43,14 @@ __device__ inline uint32_t ord_key(float x) {
 // a round's loads issued before any is used; the counts are summed per wave from ballots and
 // reduced across the block once; the position-ordered ranking of members equal to the cut
 // key (two barriers per slab) only runs when some of them must be left out.
-template <int NT, int CAP, int BITS>
+template <int NT, int CAP>
 __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
   static_assert(CAP % NT == 0 && CAP % 64 == 0, "the cache holds whole slabs");
   constexpr int U = 8;
   constexpr int NW = NT / 64;
   __shared__ int s_wave[NW];
   __shared__ int s_red[4][NW];
-  __shared__ int s_hist[SelDigits<BITS>::BINS];
+  __shared__ int s_hist[kSelBins];
   __shared__ int s_pick[3];
   __shared__ float s_b[CAP > 0 ? CAP : 1];
   __shared__ uint32_t s_r[CAP > 0 ? CAP / 32 : 1];
@@ -89,7 +89,7 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
     for (int i = tid; i < CAP; i += NT) s_b[i] = __uint_as_float(~0u);
     for (int i = tid; i < CAP / 32; i += NT) s_r[i] = ~0u;
   }
-  for (int i = tid; i < SelDigits<BITS>::BINS; i += NT) s_hist[i] = -1;
+  for (int i = tid; i < kSelBins; i += NT) s_hist[i] = -1;
   __syncthreads();
 #endif
   // ---- pass 1: counts (and the LDS copy), U slabs of NT tokens per round ----
@@ -162,8 +162,7 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
       key = ~ord_key(x);
       return is_donor(t, x, r);
     };
-    key_cut = block_select<NT, decltype(member), BITS>(len, m, member, s_hist, s_wave, s_pick,
-                                                       take_eq, &eq_total);
+    key_cut = block_select<NT>(len, m, member, s_hist, s_wave, s_pick, take_eq, &eq_total);
   }
   // every member equal to the cut key is taken unless some must be left out
   const bool rank_eq = (sel_o || sel_d) && take_eq < eq_total;
@@ -245,6 +244,226 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
   }
 }
 
+// Short sequences (at most kShortLen tokens): every thread keeps its kShortLen / NT tokens
+// (token u * NT + tid in slot u) in registers for the whole problem, so b and S0 are read
+// from HBM once and no LDS copy is needed.  The counts are per-thread sums reduced once; when
+// one side is cut, its members' keys are compacted into LDS (one LDS atomic per wave and
+// slot, no barrier), and the four 8-bit digit passes of the selection run over those keys
+// alone.  The final pass decides every token from the registers; members equal to the cut
+// key are ranked by position (slot-major, then thread) only when some must be left out.
+constexpr int kShortLen = 4096;
+
+template <int NT>
+__global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
+  constexpr int U = kShortLen / NT;
+  constexpr int NW = NT / 64;
+  static_assert(U <= 32, "the S0 and member bits of a thread's slots fit one word each");
+  __shared__ uint32_t s_key[kShortLen];
+  __shared__ int s_hist[256];
+  __shared__ uint64_t s_red[NW];
+  __shared__ int s_wave[NW];
+  __shared__ int s_pick[3];
+  __shared__ int s_n;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const int q = blockIdx.x;
+  const int h = q / a.n_seqs;
+  const int s = q - h * a.n_seqs;
+  const SeqInfo si = a.seqtab[s];
+  const int len = si.len;
+  const int64_t base = (int64_t)h * a.T + si.start;
+  const float* b = a.b + base;
+  const uint8_t* s0 = a.s0 + base;
+  uint8_t* s1 = a.s1 + base;
+  const float tau = a.tau;
+  const int rec0 = len - a.n_recent;
+  auto is_orphan = [&](int t, float x, bool r) { return !r && x < tau; };
+  auto is_donor = [&](int t, float x, bool r) {
+    return r && !(t < a.n_sink || t >= rec0) && x >= tau;
+  };
+
+#ifdef TWINKV_DEBUG
+  for (int i = tid; i < kShortLen; i += NT) s_key[i] = ~0u;
+  for (int i = tid; i < 256; i += NT) s_hist[i] = -1;
+#endif
+  if (tid == 0) s_n = 0;
+
+  // ---- load (all loads of a thread in flight together) and count ----
+  float x[U];
+  uint32_t rb = 0u;  // bit u: token u * NT + tid is in S0
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = u * NT + tid;
+    x[u] = t < len ? b[t] : 0.0f;
+    rb |= (uint32_t)(t < len && s0[t] != 0) << u;
+  }
+  int c_ret = 0, c_o = 0, c_d = 0, bad = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = u * NT + tid;
+    const bool valid = t < len;
+    const bool r = (rb >> u) & 1u;
+    c_ret += r;
+    c_o += valid && is_orphan(t, x[u], r);
+    c_d += valid && is_donor(t, x[u], r);
+    bad |= valid && !(fabsf(x[u]) <= 3.4e38f);
+  }
+  // one 64-bit word per thread (16 bits a count: a block sums at most kShortLen), summed
+  // over the wave and then over the waves
+  uint64_t pk = (uint64_t)c_ret | ((uint64_t)c_o << 16) | ((uint64_t)c_d << 32) |
+                ((uint64_t)bad << 48);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) pk += __shfl_xor(pk, off);
+  if (lane == 0) s_red[wave] = pk;
+  __syncthreads();
+  uint64_t tot = 0;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) tot += s_red[k];
+  const int tot_ret = (int)(tot & 0xFFFFu), tot_o = (int)((tot >> 16) & 0xFFFFu);
+  const int tot_d = (int)((tot >> 32) & 0xFFFFu);
+  const bool tot_bad = ((tot >> 48) & 0xFFFFu) != 0;
+
+  int status = 0;
+  if (tot_bad || (a.pmeta && (a.pmeta[q].flags & kFlagNonfinite))) status = 2;
+  else if (si.budget >= 0 && tot_ret != si.budget) status = 1;
+  const int m = status == 0 ? min(tot_o, tot_d) : 0;
+  const bool sel_o = m > 0 && tot_o > m;
+  const bool sel_d = m > 0 && tot_d > m;
+
+  uint32_t key_cut = 0xFFFFFFFFu;
+  int take_eq = 0, eq_total = 0;
+  if (sel_o || sel_d) {
+    // ---- the cut side's keys, compacted into LDS (order does not matter here): the wave
+    // takes room for all its members with one LDS atomic, then each slot's members follow
+    // the members of the wave's earlier slots ----
+    uint32_t memb = 0u;  // bit u: the token of slot u is a member
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = u * NT + tid;
+      const bool r = (rb >> u) & 1u;
+      const bool mem = t < len && (sel_o ? is_orphan(t, x[u], r) : is_donor(t, x[u], r));
+      memb |= (uint32_t)mem << u;
+    }
+    int wave_total = 0;
+    uint64_t bal[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      bal[u] = __ballot((memb >> u) & 1u);
+      wave_total += (int)__popcll(bal[u]);
+    }
+    int k0 = 0;
+    if (lane == 0 && wave_total > 0) k0 = atomicAdd(&s_n, wave_total);
+    k0 = __builtin_amdgcn_readfirstlane(k0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if ((memb >> u) & 1u)
+        s_key[k0 + (int)__popcll(bal[u] & below)] = sel_o ? ord_key(x[u]) : ~ord_key(x[u]);
+      k0 += (int)__popcll(bal[u]);
+    }
+    __syncthreads();
+    const int n = sel_o ? tot_o : tot_d;  // == s_n
+    // ---- radix select over the compacted keys: four 8-bit digits ----
+    uint32_t prefix = 0u, mask = 0u;
+    int kk = m;
+#pragma unroll 1
+    for (int pass = 0; pass < 4; ++pass) {
+      const int shift = 24 - 8 * pass;
+      for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
+      __syncthreads();
+      for (int i0 = 0; i0 < n; i0 += NT) {
+        const int i = i0 + tid;
+        const uint32_t key = i < n ? s_key[i] : 0u;
+        hist_add(i < n && (key & mask) == prefix, (int)((key >> shift) & 255u), s_hist);
+      }
+      __syncthreads();
+      constexpr int BPT = 256 >= NT ? 256 / NT : 1;
+      int hs[BPT], sum = 0;
+#pragma unroll
+      for (int j = 0; j < BPT; ++j) {
+        hs[j] = BPT * tid + j < 256 ? s_hist[BPT * tid + j] : 0;
+        sum += hs[j];
+      }
+      int dummy;
+      int before = sel_exclusive_scan<NT>(sum, s_wave, dummy);
+#pragma unroll
+      for (int j = 0; j < BPT; ++j) {
+        if (before < kk && kk <= before + hs[j]) {
+          s_pick[0] = BPT * tid + j;
+          s_pick[1] = before;
+          s_pick[2] = hs[j];
+        }
+        before += hs[j];
+      }
+      __syncthreads();
+      kk -= s_pick[1];
+      prefix |= (uint32_t)s_pick[0] << shift;
+      mask |= 255u << shift;
+      eq_total = s_pick[2];
+      __syncthreads();
+    }
+    key_cut = prefix;
+    take_eq = kk;
+  }
+  const bool rank_eq = (sel_o || sel_d) && take_eq < eq_total;
+
+  // ---- final pass from the registers ----
+  int eq_before = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = u * NT + tid;
+    const bool valid = t < len;
+    const bool r = (rb >> u) & 1u;
+    const bool orphan = valid && is_orphan(t, x[u], r);
+    const bool donor = valid && is_donor(t, x[u], r);
+    int rank = 0;
+    if (rank_eq) {
+      // position order: slot u, then thread; uniform over the block
+      const bool eq = sel_o ? (orphan && ord_key(x[u]) == key_cut)
+                            : (donor && ~ord_key(x[u]) == key_cut);
+      const uint64_t bal = __ballot(eq);
+      if (lane == 0) s_wave[wave] = (int)__popcll(bal);
+      __syncthreads();
+      rank = eq_before + (int)__popcll(bal & below);
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        const int c = s_wave[k];
+        rank += k < wave ? c : 0;
+        eq_before += c;
+      }
+      __syncthreads();
+    }
+    uint8_t out = r ? 1 : 0;
+    if (m > 0) {
+      if (orphan) {
+        bool admit = true;
+        if (sel_o) {
+          const uint32_t key = ord_key(x[u]);
+          admit = key < key_cut || (key == key_cut && rank < take_eq);
+        }
+        if (admit) out = 1;
+      } else if (donor) {
+        bool evict = true;
+        if (sel_d) {
+          const uint32_t key = ~ord_key(x[u]);
+          evict = key < key_cut || (key == key_cut && rank < take_eq);
+        }
+        if (evict) out = 0;
+      }
+    }
+    if (valid) s1[t] = out;
+  }
+  if (tid == 0) {
+    int32_t* st = a.stats + 4 * (int64_t)q;
+    st[0] = status == 0 ? tot_o : 0;
+    st[1] = status == 0 ? tot_d : 0;
+    st[2] = m;
+    st[3] = status;
+  }
+}
+
 }  // namespace
 
 int launch_repair(const RepairArgs& a, void* stream) {
@@ -252,17 +471,17 @@ int launch_repair(const RepairArgs& a, void* stream) {
   if (P == 0) return hipSuccess;
   hipStream_t st = (hipStream_t)stream;
   const dim3 grid((unsigned)P);
-  // the smallest LDS copy that holds the longest sequence; short sequences with fewer
-  // threads and 8-bit digits
-  if (a.max_len <= 4096)
-    hipLaunchKernelGGL((repair_kernel<TWINKV_K3_SHORT_THREADS, 4096, TWINKV_K3_SHORT_BITS>), grid,
+  // short sequences: tokens in registers; longer ones: the smallest LDS copy that holds the
+  // longest sequence
+  if (a.max_len <= kShortLen)
+    hipLaunchKernelGGL((repair_short_kernel<TWINKV_K3_SHORT_THREADS>), grid,
                        dim3(TWINKV_K3_SHORT_THREADS), 0, st, a);
   else if (a.max_len <= 16384)
-    hipLaunchKernelGGL((repair_kernel<1024, 16384, 11>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<1024, 16384>), grid, dim3(1024), 0, st, a);
   else if (a.max_len <= 32768)
-    hipLaunchKernelGGL((repair_kernel<1024, 32768, 11>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<1024, 32768>), grid, dim3(1024), 0, st, a);
   else
-    hipLaunchKernelGGL((repair_kernel<1024, 0, 11>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<1024, 0>), grid, dim3(1024), 0, st, a);
   return hipGetLastError();
 }
 
