@@ -22,6 +22,9 @@
 
 // Threads per problem of the short-sequence path (build-time tuning; 256 measured best
 // against 128 and 512 on 1k-4k-token sequences).
+#ifndef TWINKV_K3_16K_LDS_KEYS
+#define TWINKV_K3_16K_LDS_KEYS false
+#endif
 #ifndef TWINKV_K3_SHORT_THREADS
 #define TWINKV_K3_SHORT_THREADS 256
 #endif
@@ -464,6 +467,225 @@ __global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
   }
 }
 
+
+// Raw buffer loads whose range check returns 0 past the last byte of the sequence: the loads
+// of a thread's slots need no branches.
+constexpr int kRawBufferFlags = 0x00020000;  // 32-bit data format, gfx9 family
+__device__ inline __amdgpu_buffer_rsrc_t seq_rsrc(const void* base, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes,
+                                           kRawBufferFlags);
+}
+
+// Sequences of up to NT * U tokens with every token in registers (token u * NT + tid in slot
+// u of thread tid) and no LDS copy: the three 11/11/10-bit digit passes of the selection read
+// the registers, and LDS holds only the 2048-bin histogram, so a 36 x 8 x 32k cache does not
+// wait for LDS to free up between problems.  A slot keeps the order-preserving key of b_t
+// (orphan: b_t < tau, i.e. key < key(tau); donor: key >= key(tau)), never the float itself.
+template <int NT, int U, bool KL>
+__global__ __launch_bounds__(NT) void repair_reg_kernel(RepairArgs a) {
+  constexpr int NW = NT / 64;
+  static_assert(U <= 32, "the S0 and member bits of a thread's slots fit one word each");
+  static_assert((int64_t)NT * U < 65536, "the packed 16-bit counts hold a problem's sums");
+  __shared__ int s_hist[kSelBins];
+  // keys in LDS (KL) instead of registers: slot u of thread tid at s_key[u * NT + tid]
+  __shared__ uint32_t s_key[KL ? NT * U : 1];
+  __shared__ uint64_t s_red[NW];
+  __shared__ int s_wave[NW];
+  __shared__ int s_pick[3];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const int q = blockIdx.x;
+  const int h = q / a.n_seqs;
+  const int s = q - h * a.n_seqs;
+  const SeqInfo si = a.seqtab[s];
+  const int len = si.len;
+  const int64_t base = (int64_t)h * a.T + si.start;
+  uint8_t* s1 = a.s1 + base;
+  const uint32_t ktau = ord_key(a.tau);
+  const int rec0 = len - a.n_recent;
+  auto prot = [&](int t) { return t < a.n_sink || t >= rec0; };
+
+#ifdef TWINKV_DEBUG
+  for (int i = tid; i < kSelBins; i += NT) s_hist[i] = -1;
+#endif
+
+  // ---- load (all loads of a thread in flight together, none past the sequence) and count
+  // With the keys in LDS a slot index need not be a constant, so the slot loops unroll
+  // partially (UR slots at a time) and the loads go in batches of LB.
+  constexpr int UR = KL ? 4 : U;
+  constexpr int LB = KL ? 8 : U;
+  uint32_t kr[KL ? 1 : U];  // order-preserving keys of b (in registers unless KL)
+  auto key_of = [&](int u) -> uint32_t {
+    if constexpr (KL) return s_key[u * NT + tid];
+    else return kr[u];
+  };
+  uint32_t rb = 0u;  // bit u: token u * NT + tid is in S0
+  uint32_t orph = 0u, don = 0u;  // bit u: the token of slot u is an orphan / a donor
+  int bad = 0;
+  {
+    const __amdgpu_buffer_rsrc_t rs_b = seq_rsrc(a.b + base, 4 * len);
+    const __amdgpu_buffer_rsrc_t rs_r = seq_rsrc(a.s0 + base, len);
+#pragma unroll
+    for (int u0 = 0; u0 < U; u0 += LB) {
+      float x[LB];
+#pragma unroll
+      for (int v = 0; v < LB; ++v) {
+        const int t = (u0 + v) * NT + tid;
+        x[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs_b, 4 * t, 0, 0));
+        rb |= (uint32_t)(__builtin_amdgcn_raw_buffer_load_b8(rs_r, t, 0, 0) != 0) << (u0 + v);
+      }
+#pragma unroll
+      for (int v = 0; v < LB; ++v) {
+        const int u = u0 + v;
+        const int t = u * NT + tid;
+        const bool valid = t < len;
+        const bool r = (rb >> u) & 1u;
+        const uint32_t ku = ord_key(x[v]);
+        bad |= !(fabsf(x[v]) <= 3.4e38f);  // slots past the end hold 0
+        orph |= (uint32_t)(valid && !r && ku < ktau) << u;
+        don |= (uint32_t)(valid && r && !prot(t) && ku >= ktau) << u;
+        if constexpr (KL) s_key[u * NT + tid] = ku;
+        else kr[u] = ku;
+      }
+    }
+  }
+  const int c_ret = __builtin_popcount(rb), c_o = __builtin_popcount(orph);
+  const int c_d = __builtin_popcount(don);
+  uint64_t pk = (uint64_t)c_ret | ((uint64_t)c_o << 16) | ((uint64_t)c_d << 32) |
+                ((uint64_t)bad << 48);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) pk += __shfl_xor(pk, off);
+  if (lane == 0) s_red[wave] = pk;
+  __syncthreads();
+  uint64_t tot = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) tot += s_red[w];
+  const int tot_ret = (int)(tot & 0xFFFFu), tot_o = (int)((tot >> 16) & 0xFFFFu);
+  const int tot_d = (int)((tot >> 32) & 0xFFFFu);
+  const bool tot_bad = ((tot >> 48) & 0xFFFFu) != 0;
+
+  int status = 0;
+  if (tot_bad || (a.pmeta && (a.pmeta[q].flags & kFlagNonfinite))) status = 2;
+  else if (si.budget >= 0 && tot_ret != si.budget) status = 1;
+  const int m = status == 0 ? min(tot_o, tot_d) : 0;
+  const bool sel_o = m > 0 && tot_o > m;
+  const bool sel_d = m > 0 && tot_d > m;
+  // the cut side's members and their selection keys: ascending b for orphans, descending b
+  // for donors (the key complemented)
+  const uint32_t memb = sel_o ? orph : don;
+  const uint32_t flip = sel_o ? 0u : ~0u;
+
+  uint32_t key_cut = 0xFFFFFFFFu;
+  int take_eq = 0, eq_total = 0;
+  if (sel_o || sel_d) {
+    // ---- MSB-first radix select over the registers: 11/11/10-bit digits ----
+    using Dg = SelDigits;
+    uint32_t prefix = 0u, mask = 0u;
+    int kk = m;
+#pragma unroll 1
+    for (int pass = 0; pass < Dg::PASSES; ++pass) {
+      const int shift = Dg::shift(pass);
+      const uint32_t dmask = (1u << Dg::width(pass)) - 1u;
+      for (int i = tid; i < Dg::BINS; i += NT) s_hist[i] = 0;
+      // opaque per pass: the slots' keys and member tests are made inside the pass, not
+      // hoisted out of it into registers held for all slots
+      uint32_t fl = flip, mb = memb;
+      asm volatile("" : "+v"(fl), "+v"(mb));
+      __syncthreads();
+#pragma unroll UR
+      for (int u = 0; u < U; ++u) {
+        const uint32_t key = key_of(u) ^ fl;
+        hist_add(((mb >> u) & 1u) && (key & mask) == prefix, (int)((key >> shift) & dmask),
+                 s_hist);
+      }
+      __syncthreads();
+      constexpr int BPT = Dg::BINS >= NT ? Dg::BINS / NT : 1;
+      int hs[BPT], sum = 0;
+#pragma unroll
+      for (int j = 0; j < BPT; ++j) {
+        hs[j] = BPT * tid + j < Dg::BINS ? s_hist[BPT * tid + j] : 0;
+        sum += hs[j];
+      }
+      int dummy;
+      int before = sel_exclusive_scan<NT>(sum, s_wave, dummy);
+#pragma unroll
+      for (int j = 0; j < BPT; ++j) {
+        if (before < kk && kk <= before + hs[j]) {
+          s_pick[0] = BPT * tid + j;
+          s_pick[1] = before;
+          s_pick[2] = hs[j];
+        }
+        before += hs[j];
+      }
+      __syncthreads();
+      kk -= s_pick[1];
+      prefix |= (uint32_t)s_pick[0] << shift;
+      mask |= dmask << shift;
+      eq_total = s_pick[2];
+      __syncthreads();
+    }
+    key_cut = prefix;
+    take_eq = kk;
+  }
+  const bool rank_eq = (sel_o || sel_d) && take_eq < eq_total;
+
+  if (m == 0) {
+    // ---- nothing moves: S1 is S0 ----
+#pragma unroll UR
+    for (int u = 0; u < U; ++u) {
+      const int t = u * NT + tid;
+      if (t < len) s1[t] = (uint8_t)((rb >> u) & 1u);
+    }
+  } else {
+  // ---- final pass from the registers ----
+  int eq_before = 0;
+#pragma unroll UR
+  for (int u = 0; u < U; ++u) {
+    const int t = u * NT + tid;
+    const bool r = (rb >> u) & 1u;
+    const bool orphan = (orph >> u) & 1u;
+    const bool donor = (don >> u) & 1u;
+    const uint32_t key = key_of(u) ^ flip;
+    int rank = 0;
+    if (rank_eq) {
+      // position order: slot u, then thread; uniform over the block
+      const bool eq = ((memb >> u) & 1u) && key == key_cut;
+      const uint64_t bal = __ballot(eq);
+      if (lane == 0) s_wave[wave] = (int)__popcll(bal);
+      __syncthreads();
+      rank = eq_before + (int)__popcll(bal & below);
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const int c = s_wave[w];
+        rank += w < wave ? c : 0;
+        eq_before += c;
+      }
+      __syncthreads();
+    }
+    // a member of the cut side is taken when its key is below the cut, or equal to it and
+    // among the first take_eq of those by position; the other side is taken whole
+    const bool cut_side = sel_o ? orphan : (sel_d ? donor : false);
+    const bool taken = !cut_side || key < key_cut || (key == key_cut && rank < take_eq);
+    uint8_t out = r ? 1 : 0;
+    if (m > 0 && taken) {
+      if (orphan) out = 1;
+      else if (donor) out = 0;
+    }
+    if (t < len) s1[t] = out;
+  }
+  }
+  if (tid == 0) {
+    int32_t* st = a.stats + 4 * (int64_t)q;
+    st[0] = status == 0 ? tot_o : 0;
+    st[1] = status == 0 ? tot_d : 0;
+    st[2] = m;
+    st[3] = status;
+  }
+}
+
 }  // namespace
 
 int launch_repair(const RepairArgs& a, void* stream) {
@@ -477,9 +699,9 @@ int launch_repair(const RepairArgs& a, void* stream) {
     hipLaunchKernelGGL((repair_short_kernel<TWINKV_K3_SHORT_THREADS>), grid,
                        dim3(TWINKV_K3_SHORT_THREADS), 0, st, a);
   else if (a.max_len <= 16384)
-    hipLaunchKernelGGL((repair_kernel<1024, 16384>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_reg_kernel<1024, 16, TWINKV_K3_16K_LDS_KEYS>), grid, dim3(1024), 0, st, a);
   else if (a.max_len <= 32768)
-    hipLaunchKernelGGL((repair_kernel<1024, 32768>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_reg_kernel<1024, 32, true>), grid, dim3(1024), 0, st, a);
   else
     hipLaunchKernelGGL((repair_kernel<1024, 0>), grid, dim3(1024), 0, st, a);
   return hipGetLastError();
