@@ -12,9 +12,12 @@
 //  * Up to 4096 tokens per sequence (repair_short_kernel, 256 threads): the tokens stay in
 //    registers, the cut side's keys are compacted into LDS and selected with four 8-bit
 //    digit passes.
-//  * Longer sequences (repair_kernel, 1024 threads): 11/11/10-bit digits over 2048 LDS bins;
-//    up to 32768 tokens, b and S0 are read from HBM once (5 bytes per token) into LDS and
-//    every later pass reads LDS; longer ones stream them from global memory on every pass.
+//  * 4097 to 32768 tokens (repair_reg_kernel, 1024 threads): b and S0 are read from HBM
+//    once, in one round of loads, into 16 or 32 slots per thread (the keys of b in registers
+//    up to 16384 tokens, in LDS beyond); 11/11/10-bit digit passes over 2048 LDS bins read
+//    the slots.
+//  * Longer sequences (repair_kernel, 1024 threads): the same digits, every pass streaming
+//    b and S0 from global memory.
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"
@@ -22,6 +25,8 @@
 
 // Threads per problem of the short-sequence path (build-time tuning; 256 measured best
 // against 128 and 512 on 1k-4k-token sequences).
+// Keys of sequences of up to 16384 tokens in LDS instead of registers (build-time tuning;
+// registers measured faster: 64 against 68 us on the 36x8x16k cache).
 #ifndef TWINKV_K3_16K_LDS_KEYS
 #define TWINKV_K3_16K_LDS_KEYS false
 #endif
@@ -38,25 +43,20 @@ __device__ inline uint32_t ord_key(float x) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// CAP > 0: the problem's b and S0 (as a bit array) are copied to LDS in the first pass, so
-// HBM is read once and the selection passes run from LDS (sequences of at most CAP tokens).
-// CAP = 0: every pass reads global memory.
+// Sequences of any length: every pass reads b and S0 from global memory.
 //
 // Latency: the count pass and the final pass take U tokens per thread per round, with all of
 // a round's loads issued before any is used; the counts are summed per wave from ballots and
 // reduced across the block once; the position-ordered ranking of members equal to the cut
 // key (two barriers per slab) only runs when some of them must be left out.
-template <int NT, int CAP>
+template <int NT>
 __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
-  static_assert(CAP % NT == 0 && CAP % 64 == 0, "the cache holds whole slabs");
   constexpr int U = 8;
   constexpr int NW = NT / 64;
   __shared__ int s_wave[NW];
   __shared__ int s_red[4][NW];
   __shared__ int s_hist[kSelBins];
   __shared__ int s_pick[3];
-  __shared__ float s_b[CAP > 0 ? CAP : 1];
-  __shared__ uint32_t s_r[CAP > 0 ? CAP / 32 : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -76,26 +76,15 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
   auto is_donor = [&](int t, float x, bool r) {
     return r && !(t < a.n_sink || t >= rec0) && x >= tau;
   };
-  auto bval = [&](int t) -> float {
-    if constexpr (CAP > 0) return s_b[t];
-    else return b[t];
-  };
-  auto rbit = [&](int t) -> bool {
-    if constexpr (CAP > 0) return (s_r[t >> 5] >> (t & 31)) & 1u;
-    else return s0[t] != 0;
-  };
+  auto bval = [&](int t) -> float { return b[t]; };
+  auto rbit = [&](int t) -> bool { return s0[t] != 0; };
 
 #ifdef TWINKV_DEBUG
-  // Debug build: the LDS copy and the histogram start as poison (NaN scores, all S0 bits set),
-  // so a read of a slot the count pass did not fill changes the result.
-  if constexpr (CAP > 0) {
-    for (int i = tid; i < CAP; i += NT) s_b[i] = __uint_as_float(~0u);
-    for (int i = tid; i < CAP / 32; i += NT) s_r[i] = ~0u;
-  }
+  // Debug build: the histogram starts as poison.
   for (int i = tid; i < kSelBins; i += NT) s_hist[i] = -1;
   __syncthreads();
 #endif
-  // ---- pass 1: counts (and the LDS copy), U slabs of NT tokens per round ----
+  // ---- pass 1: counts, U slabs of NT tokens per round ----
   // per-wave counts from ballots (wave-uniform scalars)
   int c_ret = 0, c_o = 0, c_d = 0, bad = 0;
   for (int t0 = 0; t0 < len; t0 += U * NT) {
@@ -114,14 +103,6 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
       const int t = slab + tid;
       const bool valid = t < len;
       const uint64_t rb = __ballot(r[u]);
-      if constexpr (CAP > 0) {
-        if (valid) s_b[t] = x[u];
-        if (lane == 0) {
-          const int w0 = (slab + 64 * wave) >> 5;
-          s_r[w0] = (uint32_t)rb;
-          s_r[w0 + 1] = (uint32_t)(rb >> 32);
-        }
-      }
       c_ret += (int)__popcll(rb);
       c_o += (int)__popcll(__ballot(valid && is_orphan(t, x[u], r[u])));
       c_d += (int)__popcll(__ballot(valid && is_donor(t, x[u], r[u])));
@@ -134,7 +115,7 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
     s_red[2][wave] = c_d;
     s_red[3][wave] = bad;
   }
-  __syncthreads();  // also publishes the LDS copy
+  __syncthreads();
   int tot_ret = 0, tot_o = 0, tot_d = 0, tot_bad = 0;
 #pragma unroll
   for (int k = 0; k < NW; ++k) {
@@ -247,17 +228,28 @@ __global__ __launch_bounds__(NT) void repair_kernel(RepairArgs a) {
   }
 }
 
+// Raw buffer loads whose range check returns 0 past the last byte of the sequence: the loads
+// of a thread's slots need no branches.
+constexpr int kRawBufferFlags = 0x00020000;  // 32-bit data format, gfx9 family
+__device__ inline __amdgpu_buffer_rsrc_t seq_rsrc(const void* base, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes,
+                                           kRawBufferFlags);
+}
+
 // Short sequences (at most kShortLen tokens): every thread keeps its kShortLen / NT tokens
-// (token u * NT + tid in slot u) in registers for the whole problem, so b and S0 are read
-// from HBM once and no LDS copy is needed.  The counts are per-thread sums reduced once; when
-// one side is cut, its members' keys are compacted into LDS (one LDS atomic per wave and
-// slot, no barrier), and the four 8-bit digit passes of the selection run over those keys
-// alone.  The final pass decides every token from the registers; members equal to the cut
-// key are ranked by position (slot-major, then thread) only when some must be left out.
+// (token u * NT + tid in slot u) in registers for the whole problem as order-preserving keys
+// and orphan / donor / S0 bits, so b and S0 are read from HBM once, in one round of branch-
+// free loads, and no LDS copy is needed.  The counts are popcounts reduced once; when one
+// side is cut, its members' keys are compacted into LDS (one LDS atomic per wave and slot, no
+// barrier), and the four 8-bit digit passes of the selection run over those keys alone.  The
+// final pass decides every token from the registers; members equal to the cut key are ranked
+// by position (slot-major, then thread) only when some must be left out.  At most 64 VGPRs,
+// so that 8 workgroups share a CU.  (Skipping the bits the members share, with at most three
+// 9-bit digits below them, spills at that bound and measured slower.)
 constexpr int kShortLen = 4096;
 
 template <int NT>
-__global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
+__global__ __launch_bounds__(NT, 8) void repair_short_kernel(RepairArgs a) {
   constexpr int U = kShortLen / NT;
   constexpr int NW = NT / 64;
   static_assert(U <= 32, "the S0 and member bits of a thread's slots fit one word each");
@@ -294,26 +286,35 @@ __global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
 #endif
   if (tid == 0) s_n = 0;
 
-  // ---- load (all loads of a thread in flight together) and count ----
+  // ---- load (all loads of a thread in flight together, none past the sequence; raw buffer
+  // loads return 0 there, so no branches) and count ----
   float x[U];
   uint32_t rb = 0u;  // bit u: token u * NT + tid is in S0
+  {
+    const __amdgpu_buffer_rsrc_t rs_b = seq_rsrc(b, 4 * len);
+    const __amdgpu_buffer_rsrc_t rs_r = seq_rsrc(s0, len);
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int t = u * NT + tid;
-    x[u] = t < len ? b[t] : 0.0f;
-    rb |= (uint32_t)(t < len && s0[t] != 0) << u;
+    for (int u = 0; u < U; ++u) {
+      const int t = u * NT + tid;
+      x[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs_b, 4 * t, 0, 0));
+      rb |= (uint32_t)(__builtin_amdgcn_raw_buffer_load_b8(rs_r, t, 0, 0) != 0) << u;
+    }
   }
-  int c_ret = 0, c_o = 0, c_d = 0, bad = 0;
+  uint32_t orph = 0u, don = 0u;  // bit u: the token of slot u is an orphan / a donor
+  int bad = 0;
+  uint32_t k[U];  // order-preserving keys of b (the floats are not kept)
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int t = u * NT + tid;
     const bool valid = t < len;
     const bool r = (rb >> u) & 1u;
-    c_ret += r;
-    c_o += valid && is_orphan(t, x[u], r);
-    c_d += valid && is_donor(t, x[u], r);
+    orph |= (uint32_t)(valid && is_orphan(t, x[u], r)) << u;
+    don |= (uint32_t)(valid && is_donor(t, x[u], r)) << u;
     bad |= valid && !(fabsf(x[u]) <= 3.4e38f);
+    k[u] = ord_key(x[u]);
   }
+  const int c_ret = __builtin_popcount(rb), c_o = __builtin_popcount(orph);
+  const int c_d = __builtin_popcount(don);
   // one 64-bit word per thread (16 bits a count: a block sums at most kShortLen), summed
   // over the wave and then over the waves
   uint64_t pk = (uint64_t)c_ret | ((uint64_t)c_o << 16) | ((uint64_t)c_d << 32) |
@@ -342,19 +343,12 @@ __global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
     // ---- the cut side's keys, compacted into LDS (order does not matter here): the wave
     // takes room for all its members with one LDS atomic, then each slot's members follow
     // the members of the wave's earlier slots ----
-    uint32_t memb = 0u;  // bit u: the token of slot u is a member
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int t = u * NT + tid;
-      const bool r = (rb >> u) & 1u;
-      const bool mem = t < len && (sel_o ? is_orphan(t, x[u], r) : is_donor(t, x[u], r));
-      memb |= (uint32_t)mem << u;
-    }
+    const uint32_t mbits = sel_o ? orph : don;  // bit u: the token of slot u is a member
     int wave_total = 0;
     uint64_t bal[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      bal[u] = __ballot((memb >> u) & 1u);
+      bal[u] = __ballot((mbits >> u) & 1u);
       wave_total += (int)__popcll(bal[u]);
     }
     int k0 = 0;
@@ -362,8 +356,8 @@ __global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
     k0 = __builtin_amdgcn_readfirstlane(k0);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if ((memb >> u) & 1u)
-        s_key[k0 + (int)__popcll(bal[u] & below)] = sel_o ? ord_key(x[u]) : ~ord_key(x[u]);
+      if ((mbits >> u) & 1u)
+        s_key[k0 + (int)__popcll(bal[u] & below)] = sel_o ? k[u] : ~k[u];
       k0 += (int)__popcll(bal[u]);
     }
     __syncthreads();
@@ -413,50 +407,42 @@ __global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
   const bool rank_eq = (sel_o || sel_d) && take_eq < eq_total;
 
   // ---- final pass from the registers ----
+  const uint32_t memb = sel_o ? orph : don;  // the cut side (when one side is cut)
+  const uint32_t flip = sel_o ? 0u : ~0u;
   int eq_before = 0;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int t = u * NT + tid;
-    const bool valid = t < len;
     const bool r = (rb >> u) & 1u;
-    const bool orphan = valid && is_orphan(t, x[u], r);
-    const bool donor = valid && is_donor(t, x[u], r);
+    const bool orphan = (orph >> u) & 1u;
+    const bool donor = (don >> u) & 1u;
+    const uint32_t key = k[u] ^ flip;
     int rank = 0;
     if (rank_eq) {
       // position order: slot u, then thread; uniform over the block
-      const bool eq = sel_o ? (orphan && ord_key(x[u]) == key_cut)
-                            : (donor && ~ord_key(x[u]) == key_cut);
+      const bool eq = ((memb >> u) & 1u) && key == key_cut;
       const uint64_t bal = __ballot(eq);
       if (lane == 0) s_wave[wave] = (int)__popcll(bal);
       __syncthreads();
       rank = eq_before + (int)__popcll(bal & below);
 #pragma unroll
-      for (int k = 0; k < NW; ++k) {
-        const int c = s_wave[k];
-        rank += k < wave ? c : 0;
+      for (int w = 0; w < NW; ++w) {
+        const int c = s_wave[w];
+        rank += w < wave ? c : 0;
         eq_before += c;
       }
       __syncthreads();
     }
+    // a member of the cut side is taken when its key is below the cut, or equal to it and
+    // among the first take_eq of those by position; the other side is taken whole
+    const bool cut_side = sel_o ? orphan : (sel_d ? donor : false);
+    const bool taken = !cut_side || key < key_cut || (key == key_cut && rank < take_eq);
     uint8_t out = r ? 1 : 0;
-    if (m > 0) {
-      if (orphan) {
-        bool admit = true;
-        if (sel_o) {
-          const uint32_t key = ord_key(x[u]);
-          admit = key < key_cut || (key == key_cut && rank < take_eq);
-        }
-        if (admit) out = 1;
-      } else if (donor) {
-        bool evict = true;
-        if (sel_d) {
-          const uint32_t key = ~ord_key(x[u]);
-          evict = key < key_cut || (key == key_cut && rank < take_eq);
-        }
-        if (evict) out = 0;
-      }
+    if (m > 0 && taken) {
+      if (orphan) out = 1;
+      else if (donor) out = 0;
     }
-    if (valid) s1[t] = out;
+    if (t < len) s1[t] = out;
   }
   if (tid == 0) {
     int32_t* st = a.stats + 4 * (int64_t)q;
@@ -467,14 +453,6 @@ __global__ __launch_bounds__(NT) void repair_short_kernel(RepairArgs a) {
   }
 }
 
-
-// Raw buffer loads whose range check returns 0 past the last byte of the sequence: the loads
-// of a thread's slots need no branches.
-constexpr int kRawBufferFlags = 0x00020000;  // 32-bit data format, gfx9 family
-__device__ inline __amdgpu_buffer_rsrc_t seq_rsrc(const void* base, int nbytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes,
-                                           kRawBufferFlags);
-}
 
 // Sequences of up to NT * U tokens with every token in registers (token u * NT + tid in slot
 // u of thread tid) and no LDS copy: the three 11/11/10-bit digit passes of the selection read
@@ -693,17 +671,17 @@ int launch_repair(const RepairArgs& a, void* stream) {
   if (P == 0) return hipSuccess;
   hipStream_t st = (hipStream_t)stream;
   const dim3 grid((unsigned)P);
-  // short sequences: tokens in registers; longer ones: the smallest LDS copy that holds the
-  // longest sequence
+  // the smallest kernel whose slots hold the longest sequence; beyond 32768 tokens, streaming
   if (a.max_len <= kShortLen)
     hipLaunchKernelGGL((repair_short_kernel<TWINKV_K3_SHORT_THREADS>), grid,
                        dim3(TWINKV_K3_SHORT_THREADS), 0, st, a);
   else if (a.max_len <= 16384)
-    hipLaunchKernelGGL((repair_reg_kernel<1024, 16, TWINKV_K3_16K_LDS_KEYS>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_reg_kernel<1024, 16, TWINKV_K3_16K_LDS_KEYS>), grid, dim3(1024),
+                       0, st, a);
   else if (a.max_len <= 32768)
     hipLaunchKernelGGL((repair_reg_kernel<1024, 32, true>), grid, dim3(1024), 0, st, a);
   else
-    hipLaunchKernelGGL((repair_kernel<1024, 0>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((repair_kernel<1024>), grid, dim3(1024), 0, st, a);
   return hipGetLastError();
 }
 
