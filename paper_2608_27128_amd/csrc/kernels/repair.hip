@@ -10,8 +10,8 @@
 // a pass in position order that takes exactly the remaining members equal to that key
 // (ranked by wave ballots) when some of them must be left out.
 //  * Up to 4096 tokens per sequence (repair_short_kernel, 256 threads): the tokens stay in
-//    registers, the cut side's keys are compacted into LDS and selected with four 8-bit
-//    digit passes.
+//    registers, the cut side's keys are compacted into LDS and selected with 8-bit digit
+//    passes below the leading bits they all share.
 //  * 4097 to 32768 tokens (repair_reg_kernel, 1024 threads): b and S0 are read from HBM
 //    once, in one round of loads, into 16 or 32 slots per thread (the keys of b in registers
 //    up to 16384 tokens, in LDS beyond); 11/11/10-bit digit passes over 2048 LDS bins read
@@ -239,26 +239,32 @@ __device__ inline __amdgpu_buffer_rsrc_t seq_rsrc(const void* base, int nbytes) 
 // Short sequences (at most kShortLen tokens): every thread keeps its kShortLen / NT tokens
 // (token u * NT + tid in slot u) in registers for the whole problem as order-preserving keys
 // and orphan / donor / S0 bits, so b and S0 are read from HBM once, in one round of branch-
-// free loads, and no LDS copy is needed.  The counts are popcounts reduced once; when one
-// side is cut, its members' keys are compacted into LDS (one LDS atomic per wave and slot, no
-// barrier), and the four 8-bit digit passes of the selection run over those keys alone.  The
-// final pass decides every token from the registers; members equal to the cut key are ranked
-// by position (slot-major, then thread) only when some must be left out.  At most 64 VGPRs,
-// so that 8 workgroups share a CU.  (Skipping the bits the members share, with at most three
-// 9-bit digits below them, spills at that bound and measured slower.)
+// free loads, and no LDS copy is needed.  The counts are popcounts reduced once.  When one
+// side is cut, each wave compacts its members' keys into its own part of LDS (ballots, no
+// atomics); the AND and OR of all of them give the leading bits they share, and the
+// selection runs 8-bit digit passes over the bits below those only, each with two barriers
+// (one wave scans the histogram while another clears the next one), stopping once the
+// bucket of the m-th key is taken whole.  The final pass decides every token from the
+// registers; members equal to the cut key are ranked by position (slot-major, then thread)
+// only when some must be left out.  At most 64 VGPRs, so that 8 workgroups share a CU.
+// (Layouts with runs of 4 or 16 consecutive tokens per thread, read with 16-byte loads,
+// measured slower: a problem's rows are rarely 16-byte aligned.)
 constexpr int kShortLen = 4096;
 
 template <int NT>
 __global__ __launch_bounds__(NT, 8) void repair_short_kernel(RepairArgs a) {
   constexpr int U = kShortLen / NT;
   constexpr int NW = NT / 64;
+  constexpr int WCAP = 64 * U;  // members one wave can hold
   static_assert(U <= 32, "the S0 and member bits of a thread's slots fit one word each");
+  static_assert(NW >= 2, "one wave scans the histogram while another clears the next one");
+  // wave w's members of the cut side at s_key[w * WCAP, w * WCAP + its count)
   __shared__ uint32_t s_key[kShortLen];
-  __shared__ int s_hist[256];
+  __shared__ int s_hist[2][256];  // digit histograms, used in turn
   __shared__ uint64_t s_red[NW];
+  __shared__ uint32_t s_bits[NW][2];  // per wave: AND and OR of its members' keys
   __shared__ int s_wave[NW];
   __shared__ int s_pick[3];
-  __shared__ int s_n;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -282,9 +288,9 @@ __global__ __launch_bounds__(NT, 8) void repair_short_kernel(RepairArgs a) {
 
 #ifdef TWINKV_DEBUG
   for (int i = tid; i < kShortLen; i += NT) s_key[i] = ~0u;
-  for (int i = tid; i < 256; i += NT) s_hist[i] = -1;
+  for (int i = tid; i < 256; i += NT) s_hist[1][i] = -1;
 #endif
-  if (tid == 0) s_n = 0;
+  for (int i = tid; i < 256; i += NT) s_hist[0][i] = 0;  // visible after the count barrier
 
   // ---- load (all loads of a thread in flight together, none past the sequence; raw buffer
   // loads return 0 there, so no branches) and count ----
@@ -340,73 +346,112 @@ __global__ __launch_bounds__(NT, 8) void repair_short_kernel(RepairArgs a) {
   uint32_t key_cut = 0xFFFFFFFFu;
   int take_eq = 0, eq_total = 0;
   if (sel_o || sel_d) {
-    // ---- the cut side's keys, compacted into LDS (order does not matter here): the wave
-    // takes room for all its members with one LDS atomic, then each slot's members follow
-    // the members of the wave's earlier slots ----
+    // ---- the cut side's keys (descending donors as complemented keys), compacted per wave
+    // into the wave's own part of LDS, in no particular order; the AND and the OR of all of
+    // them give the leading bits they share, which no digit pass needs to look at ----
     const uint32_t mbits = sel_o ? orph : don;  // bit u: the token of slot u is a member
-    int wave_total = 0;
-    uint64_t bal[U];
+    const uint32_t flip = sel_o ? 0u : ~0u;
+    uint32_t* wkeys = s_key + wave * WCAP;
+    int nmem = 0;  // members of this wave so far (uniform over the wave)
+    uint32_t kand = ~0u, kor = 0u;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      bal[u] = __ballot((mbits >> u) & 1u);
-      wave_total += (int)__popcll(bal[u]);
+      const bool mem = (mbits >> u) & 1u;
+      const uint64_t bal = __ballot(mem);
+      const uint32_t key = k[u] ^ flip;
+      if (mem) {
+        wkeys[nmem + (int)__popcll(bal & below)] = key;
+        kand &= key;
+        kor |= key;
+      }
+      nmem += (int)__popcll(bal);
     }
-    int k0 = 0;
-    if (lane == 0 && wave_total > 0) k0 = atomicAdd(&s_n, wave_total);
-    k0 = __builtin_amdgcn_readfirstlane(k0);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if ((mbits >> u) & 1u)
-        s_key[k0 + (int)__popcll(bal[u] & below)] = sel_o ? k[u] : ~k[u];
-      k0 += (int)__popcll(bal[u]);
+    for (int off = 32; off >= 1; off >>= 1) {
+      kand &= __shfl_xor(kand, off);
+      kor |= __shfl_xor(kor, off);
+    }
+    if (lane == 0) {
+      s_bits[wave][0] = kand;
+      s_bits[wave][1] = kor;
     }
     __syncthreads();
-    const int n = sel_o ? tot_o : tot_d;  // == s_n
-    // ---- radix select over the compacted keys: four 8-bit digits ----
-    uint32_t prefix = 0u, mask = 0u;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      kand &= s_bits[w][0];
+      kor |= s_bits[w][1];
+    }
+    // ---- radix select, MSB first, in digits of up to 8 bits below the shared bits: after
+    // each pass, bits [hi, 32) of the kk-th smallest key are known (prefix) and cnt members
+    // share them.  The passes stop early once every one of those cnt is taken. ----
+    const uint32_t diff = kand ^ kor;
+    int hi = diff ? 32 - __clz(diff) : 0;
+    uint32_t mask = hi >= 32 ? 0u : (~0u << hi);
+    uint32_t prefix = kand & mask;
     int kk = m;
+    int cnt = sel_o ? tot_o : tot_d;
+    int buf = 0;
 #pragma unroll 1
-    for (int pass = 0; pass < 4; ++pass) {
-      const int shift = 24 - 8 * pass;
-      for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
-      __syncthreads();
-      for (int i0 = 0; i0 < n; i0 += NT) {
-        const int i = i0 + tid;
-        const uint32_t key = i < n ? s_key[i] : 0u;
-        hist_add(i < n && (key & mask) == prefix, (int)((key >> shift) & 255u), s_hist);
-      }
-      __syncthreads();
-      constexpr int BPT = 256 >= NT ? 256 / NT : 1;
-      int hs[BPT], sum = 0;
-#pragma unroll
-      for (int j = 0; j < BPT; ++j) {
-        hs[j] = BPT * tid + j < 256 ? s_hist[BPT * tid + j] : 0;
-        sum += hs[j];
-      }
-      int dummy;
-      int before = sel_exclusive_scan<NT>(sum, s_wave, dummy);
-#pragma unroll
-      for (int j = 0; j < BPT; ++j) {
-        if (before < kk && kk <= before + hs[j]) {
-          s_pick[0] = BPT * tid + j;
-          s_pick[1] = before;
-          s_pick[2] = hs[j];
+    while (hi > 0 && kk < cnt) {
+      const int shift = hi > 8 ? hi - 8 : 0;
+      const uint32_t dmask = (1u << (hi - shift)) - 1u;
+      for (int i0 = 0; i0 < nmem; i0 += 64) {
+        const int i = i0 + lane;
+        if (i < nmem) {
+          const uint32_t key = wkeys[i];
+          if ((key & mask) == prefix) atomicAdd(&s_hist[buf][(key >> shift) & dmask], 1);
         }
-        before += hs[j];
+      }
+      __syncthreads();
+      if (wave == 0) {
+        // bins 4 lane .. 4 lane + 3; the lane whose range holds the kk-th key picks its bin
+        const int4 h4 = *reinterpret_cast<const int4*>(&s_hist[buf][4 * lane]);
+        const int sum = h4.x + h4.y + h4.z + h4.w;
+        int inc = sum;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const int y = __shfl_up(inc, off);
+          if (lane >= off) inc += y;
+        }
+        int before = inc - sum;
+        if (before < kk && kk <= inc) {
+          int bin = 4 * lane, c = h4.x;
+          if (kk > before + c) { before += c; ++bin; c = h4.y; }
+          if (kk > before + c) { before += c; ++bin; c = h4.z; }
+          if (kk > before + c) { before += c; ++bin; c = h4.w; }
+          s_pick[0] = bin;
+          s_pick[1] = before;
+          s_pick[2] = c;
+        }
+      } else if (wave == 1) {
+        // the next pass's histogram
+        *reinterpret_cast<int4*>(&s_hist[buf ^ 1][4 * lane]) = make_int4(0, 0, 0, 0);
       }
       __syncthreads();
       kk -= s_pick[1];
       prefix |= (uint32_t)s_pick[0] << shift;
-      mask |= 255u << shift;
-      eq_total = s_pick[2];
-      __syncthreads();
+      mask |= dmask << shift;
+      cnt = s_pick[2];
+      hi = shift;
+      buf ^= 1;
     }
-    key_cut = prefix;
-    take_eq = kk;
+    if (kk == cnt) {
+      // every member sharing bits [hi, 32) with the kk-th key is taken: cut at the largest
+      // key with those bits, all members equal to it taken
+      key_cut = prefix | ~mask;
+      take_eq = cnt;
+    } else {
+      key_cut = prefix;  // hi == 0: the kk-th key itself; cnt members equal it
+      take_eq = kk;
+    }
+    eq_total = cnt;
   }
   const bool rank_eq = (sel_o || sel_d) && take_eq < eq_total;
 
   // ---- final pass from the registers ----
+  // (opaque: the slots' bits are read back from the three words, instead of the compiler
+  // keeping the per-slot predicates of the load phase alive, and spilled, until here)
+  asm volatile("" : "+v"(rb), "+v"(orph), "+v"(don));
   const uint32_t memb = sel_o ? orph : don;  // the cut side (when one side is cut)
   const uint32_t flip = sel_o ? 0u : ~0u;
   int eq_before = 0;
