@@ -14,8 +14,8 @@
 //    passes below the leading bits they all share.
 //  * 4097 to 32768 tokens (repair_reg_kernel, 1024 threads): b and S0 are read from HBM
 //    once, in one round of loads, into 16 or 32 slots per thread (the keys of b in registers
-//    up to 16384 tokens, in LDS beyond); 11/11/10-bit digit passes over 2048 LDS bins read
-//    the slots.
+//    up to 16384 tokens, in LDS beyond); digit passes of up to 11 bits over 2048 LDS bins,
+//    below the leading bits the cut side's keys share, read the slots.
 //  * Longer sequences (repair_kernel, 1024 threads): the same digits, every pass streaming
 //    b and S0 from global memory.
 #include <hip/hip_runtime.h>
@@ -499,20 +499,25 @@ __global__ __launch_bounds__(NT, 8) void repair_short_kernel(RepairArgs a) {
 }
 
 
-// Sequences of up to NT * U tokens with every token in registers (token u * NT + tid in slot
-// u of thread tid) and no LDS copy: the three 11/11/10-bit digit passes of the selection read
-// the registers, and LDS holds only the 2048-bin histogram, so a 36 x 8 x 32k cache does not
-// wait for LDS to free up between problems.  A slot keeps the order-preserving key of b_t
-// (orphan: b_t < tau, i.e. key < key(tau); donor: key >= key(tau)), never the float itself.
+// Sequences of up to NT * U tokens with every token in a slot of its own thread (token
+// u * NT + tid in slot u of thread tid): in registers, or (KL) in an LDS array that b is
+// loaded into directly.  A slot keeps the order-preserving key of b_t (orphan: b_t < tau, i.e.
+// key < key(tau); donor: key >= key(tau)), never the float itself.  When one side is cut, the
+// AND and OR of its keys give the leading bits they all share, and the selection's digit
+// passes (up to 11 bits, 2048 LDS bins, two barriers each: one wave scans the histogram while
+// another clears the next one) start below those bits and stop once the bucket of the m-th
+// key is taken whole.  When m = 0 the final pass copies S0.
 template <int NT, int U, bool KL>
 __global__ __launch_bounds__(NT) void repair_reg_kernel(RepairArgs a) {
   constexpr int NW = NT / 64;
   static_assert(U <= 32, "the S0 and member bits of a thread's slots fit one word each");
   static_assert((int64_t)NT * U < 65536, "the packed 16-bit counts hold a problem's sums");
-  __shared__ int s_hist[kSelBins];
+  static_assert(NW >= 2, "one wave scans the histogram while another clears the next one");
+  __shared__ int s_hist[2][kSelBins];  // digit histograms, used in turn
   // keys in LDS (KL) instead of registers: slot u of thread tid at s_key[u * NT + tid]
   __shared__ uint32_t s_key[KL ? NT * U : 1];
   __shared__ uint64_t s_red[NW];
+  __shared__ uint32_t s_bits[NW][2];  // per wave: AND and OR of its members' keys
   __shared__ int s_wave[NW];
   __shared__ int s_pick[3];
 
@@ -532,14 +537,15 @@ __global__ __launch_bounds__(NT) void repair_reg_kernel(RepairArgs a) {
   auto prot = [&](int t) { return t < a.n_sink || t >= rec0; };
 
 #ifdef TWINKV_DEBUG
-  for (int i = tid; i < kSelBins; i += NT) s_hist[i] = -1;
+  for (int i = tid; i < kSelBins; i += NT) s_hist[1][i] = -1;
 #endif
+  for (int i = tid; i < kSelBins; i += NT) s_hist[0][i] = 0;  // visible after the count barrier
 
-  // ---- load (all loads of a thread in flight together, none past the sequence) and count
-  // With the keys in LDS a slot index need not be a constant, so the slot loops unroll
-  // partially (UR slots at a time) and the loads go in batches of LB.
+  // ---- load (all loads of a thread in flight together, none past the sequence) and count.
+  // With the keys in LDS, b goes straight into s_key by 4-byte direct loads (no registers,
+  // one round with the S0 bytes) and is turned into keys in place; a slot index then need not
+  // be a constant, so the slot loops unroll partially (UR slots at a time).
   constexpr int UR = KL ? 4 : U;
-  constexpr int LB = KL ? 8 : U;
   uint32_t kr[KL ? 1 : U];  // order-preserving keys of b (in registers unless KL)
   auto key_of = [&](int u) -> uint32_t {
     if constexpr (KL) return s_key[u * NT + tid];
@@ -551,28 +557,35 @@ __global__ __launch_bounds__(NT) void repair_reg_kernel(RepairArgs a) {
   {
     const __amdgpu_buffer_rsrc_t rs_b = seq_rsrc(a.b + base, 4 * len);
     const __amdgpu_buffer_rsrc_t rs_r = seq_rsrc(a.s0 + base, len);
+    float x[KL ? 1 : U];
 #pragma unroll
-    for (int u0 = 0; u0 < U; u0 += LB) {
-      float x[LB];
-#pragma unroll
-      for (int v = 0; v < LB; ++v) {
-        const int t = (u0 + v) * NT + tid;
-        x[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs_b, 4 * t, 0, 0));
-        rb |= (uint32_t)(__builtin_amdgcn_raw_buffer_load_b8(rs_r, t, 0, 0) != 0) << (u0 + v);
+    for (int u = 0; u < U; ++u) {
+      const int t = u * NT + tid;
+      if constexpr (KL) {
+        // lane l of the wave lands at s_key[u * NT + 64 wave + l], its own slot u
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs_b, (void __attribute__((address_space(3)))*)(s_key + u * NT + 64 * wave), 4,
+            4 * t, 0, 0, 0);
+      } else {
+        x[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs_b, 4 * t, 0, 0));
       }
-#pragma unroll
-      for (int v = 0; v < LB; ++v) {
-        const int u = u0 + v;
-        const int t = u * NT + tid;
-        const bool valid = t < len;
-        const bool r = (rb >> u) & 1u;
-        const uint32_t ku = ord_key(x[v]);
-        bad |= !(fabsf(x[v]) <= 3.4e38f);  // slots past the end hold 0
-        orph |= (uint32_t)(valid && !r && ku < ktau) << u;
-        don |= (uint32_t)(valid && r && !prot(t) && ku >= ktau) << u;
-        if constexpr (KL) s_key[u * NT + tid] = ku;
-        else kr[u] = ku;
-      }
+      rb |= (uint32_t)(__builtin_amdgcn_raw_buffer_load_b8(rs_r, t, 0, 0) != 0) << u;
+    }
+    if constexpr (KL) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll UR
+    for (int u = 0; u < U; ++u) {
+      const int t = u * NT + tid;
+      const bool valid = t < len;
+      const bool r = (rb >> u) & 1u;
+      float xv;
+      if constexpr (KL) xv = __uint_as_float(s_key[u * NT + tid]);
+      else xv = x[u];
+      const uint32_t ku = ord_key(xv);
+      bad |= !(fabsf(xv) <= 3.4e38f);  // slots past the end hold 0
+      orph |= (uint32_t)(valid && !r && ku < ktau) << u;
+      don |= (uint32_t)(valid && r && !prot(t) && ku >= ktau) << u;
+      if constexpr (KL) s_key[u * NT + tid] = ku;
+      else kr[u] = ku;
     }
   }
   const int c_ret = __builtin_popcount(rb), c_o = __builtin_popcount(orph);
@@ -604,54 +617,122 @@ __global__ __launch_bounds__(NT) void repair_reg_kernel(RepairArgs a) {
   uint32_t key_cut = 0xFFFFFFFFu;
   int take_eq = 0, eq_total = 0;
   if (sel_o || sel_d) {
-    // ---- MSB-first radix select over the registers: 11/11/10-bit digits ----
-    using Dg = SelDigits;
-    uint32_t prefix = 0u, mask = 0u;
-    int kk = m;
-#pragma unroll 1
-    for (int pass = 0; pass < Dg::PASSES; ++pass) {
-      const int shift = Dg::shift(pass);
-      const uint32_t dmask = (1u << Dg::width(pass)) - 1u;
-      for (int i = tid; i < Dg::BINS; i += NT) s_hist[i] = 0;
-      // opaque per pass: the slots' keys and member tests are made inside the pass, not
+    // ---- the AND and OR of the cut side's keys: the leading bits they all share ----
+    uint32_t kand = ~0u, kor = 0u;
+    {
+      // opaque: the slots' keys and member tests are made in each loop over the slots, not
       // hoisted out of it into registers held for all slots
       uint32_t fl = flip, mb = memb;
       asm volatile("" : "+v"(fl), "+v"(mb));
-      __syncthreads();
 #pragma unroll UR
       for (int u = 0; u < U; ++u) {
         const uint32_t key = key_of(u) ^ fl;
-        hist_add(((mb >> u) & 1u) && (key & mask) == prefix, (int)((key >> shift) & dmask),
-                 s_hist);
+        const bool mem = (mb >> u) & 1u;
+        kand &= mem ? key : ~0u;
+        kor |= mem ? key : 0u;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      kand &= __shfl_xor(kand, off);
+      kor |= __shfl_xor(kor, off);
+    }
+    if (lane == 0) {
+      s_bits[wave][0] = kand;
+      s_bits[wave][1] = kor;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      kand &= s_bits[w][0];
+      kor |= s_bits[w][1];
+    }
+    // ---- MSB-first radix select in digits of up to 11 bits below the shared bits, over the
+    // slots: after each pass bits [hi, 32) of the kk-th smallest key are known (prefix) and
+    // cnt members share them; the passes stop once every one of those cnt is taken ----
+    const uint32_t diff = kand ^ kor;
+    int hi = diff ? 32 - __clz(diff) : 0;
+    uint32_t mask = hi >= 32 ? 0u : (~0u << hi);
+    uint32_t prefix = kand & mask;
+    int kk = m;
+    int cnt = sel_o ? tot_o : tot_d;
+    int buf = 0;
+#pragma unroll 1
+    while (hi > 0 && kk < cnt) {
+      const int shift = hi > 11 ? hi - 11 : 0;
+      const uint32_t dmask = (1u << (hi - shift)) - 1u;
+      uint32_t fl = flip, mb = memb;
+      asm volatile("" : "+v"(fl), "+v"(mb));
+#pragma unroll UR
+      for (int u = 0; u < U; ++u) {
+        const uint32_t key = key_of(u) ^ fl;
+        if (((mb >> u) & 1u) && (key & mask) == prefix)
+          atomicAdd(&s_hist[buf][(key >> shift) & dmask], 1);
       }
       __syncthreads();
-      constexpr int BPT = Dg::BINS >= NT ? Dg::BINS / NT : 1;
-      int hs[BPT], sum = 0;
+      if (wave == 0) {
+        // bins 32 lane .. 32 lane + 31; the lane whose range holds the kk-th key picks its bin
+        constexpr int BPL = kSelBins / 64;
+        int hb[BPL];
+        int sum = 0;
 #pragma unroll
-      for (int j = 0; j < BPT; ++j) {
-        hs[j] = BPT * tid + j < Dg::BINS ? s_hist[BPT * tid + j] : 0;
-        sum += hs[j];
-      }
-      int dummy;
-      int before = sel_exclusive_scan<NT>(sum, s_wave, dummy);
-#pragma unroll
-      for (int j = 0; j < BPT; ++j) {
-        if (before < kk && kk <= before + hs[j]) {
-          s_pick[0] = BPT * tid + j;
-          s_pick[1] = before;
-          s_pick[2] = hs[j];
+        for (int j = 0; j < BPL / 4; ++j) {
+          const int4 h4 = *reinterpret_cast<const int4*>(&s_hist[buf][BPL * lane + 4 * j]);
+          hb[4 * j + 0] = h4.x;
+          hb[4 * j + 1] = h4.y;
+          hb[4 * j + 2] = h4.z;
+          hb[4 * j + 3] = h4.w;
+          sum += h4.x + h4.y + h4.z + h4.w;
         }
-        before += hs[j];
+        int inc = sum;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const int y = __shfl_up(inc, off);
+          if (lane >= off) inc += y;
+        }
+        int before = inc - sum;
+        if (before < kk && kk <= inc) {
+          int bin = -1, c = 0;
+#pragma unroll
+          for (int e = 0; e < BPL; ++e) {
+            if (bin < 0) {
+              if (kk <= before + hb[e]) {
+                bin = BPL * lane + e;
+                c = hb[e];
+              } else {
+                before += hb[e];
+              }
+            }
+          }
+          s_pick[0] = bin;
+          s_pick[1] = before;
+          s_pick[2] = c;
+        }
+      } else if (wave == 1) {
+        // the next pass's histogram
+#pragma unroll
+        for (int j = 0; j < kSelBins / 256; ++j)
+          *reinterpret_cast<int4*>(&s_hist[buf ^ 1][kSelBins / 64 * lane + 4 * j]) =
+              make_int4(0, 0, 0, 0);
       }
       __syncthreads();
       kk -= s_pick[1];
       prefix |= (uint32_t)s_pick[0] << shift;
       mask |= dmask << shift;
-      eq_total = s_pick[2];
-      __syncthreads();
+      cnt = s_pick[2];
+      hi = shift;
+      buf ^= 1;
     }
-    key_cut = prefix;
-    take_eq = kk;
+    if (kk == cnt) {
+      // every member sharing bits [hi, 32) with the kk-th key is taken: cut at the largest
+      // key with those bits, all members equal to it taken
+      key_cut = prefix | ~mask;
+      take_eq = cnt;
+    } else {
+      key_cut = prefix;  // hi == 0: the kk-th key itself; cnt members equal it
+      take_eq = kk;
+    }
+    eq_total = cnt;
   }
   const bool rank_eq = (sel_o || sel_d) && take_eq < eq_total;
 
