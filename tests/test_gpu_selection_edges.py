@@ -1,0 +1,106 @@
+"""Edge cases of the repair pass's selection (Sec. 3.4: the m most severe orphans and donors):
+cut-side scores that are all equal, that differ only in their last bits, that take two values
+with m falling exactly at the end of the first, that form two clusters with m falling exactly
+at the end of the first (whose scores differ in their low 12 bits, so the bucket of the m-th
+key holds many distinct keys when the selection stops early), and that span both signs.  The
+selection skips the leading bits the cut side's keys share and stops once the m-th key's
+bucket is taken whole; every case must still give the oracle's S1 and counts bit for bit, for
+each kernel (up to 4096 tokens, up to 16384, up to 32768, longer)."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import host, mask_to_device
+from paper_2608_27128_amd import binding
+
+pytestmark = pytest.mark.gpu
+
+TAU = 0.5
+N_SINK, N_RECENT = 4, 16
+KINDS = ("equal", "lowbits", "two", "cluster", "spread")
+
+
+def cut_values(kind, side, k, g):
+    """k scores for the cut side (orphans: below TAU; donors: at or above it)."""
+    base = np.float32(0.25 if side == "o" else 0.75)
+    if kind == "equal":
+        return np.full(k, base, np.float32)
+    if kind == "lowbits":
+        return (base.view(np.int32) + g.integers(0, 8, k).astype(np.int32)).view(np.float32)
+    if kind == "two":
+        hi = np.float32(0.375 if side == "o" else 0.875)
+        v = np.full(k, hi, np.float32)
+        v[: k // 2] = base
+        return v
+    if side == "o":  # spread: both signs below TAU
+        return g.uniform(-1.0, TAU, k).astype(np.float32)
+    return g.uniform(TAU, 1.0, k).astype(np.float32)
+
+
+def make_problem(n, kind, side, g):
+    """Scores b and retained set S0 of one problem whose cut side is `side` (o: orphans are
+    cut, so there are fewer donors; d: the reverse)."""
+    B = (4 * n) // 10
+    perm = g.permutation(n)
+    s0 = np.zeros(n, np.uint8)
+    s0[perm[:B]] = 1
+    ret = np.flatnonzero(s0)
+    out = np.flatnonzero(s0 == 0)
+    b = np.empty(n, np.float32)
+    # defaults: retained tokens below TAU (kept, not donors), evicted ones at or above (not
+    # orphans)
+    b[ret] = g.uniform(0.0, TAU - 0.01, ret.size).astype(np.float32)
+    b[out] = g.uniform(TAU + 0.01, 1.0, out.size).astype(np.float32)
+    orph = g.permutation(out)
+    # donors only outside the protected sink and recent regions, so that m is what is set here
+    don = g.permutation(ret[(ret >= N_SINK) & (ret < n - N_RECENT)])
+    if side == "o":
+        orph = orph[: (6 * out.size) // 10]
+        n_don = max(1, orph.size // 2 if kind in ("two", "cluster") else orph.size // 7)
+        don = don[:n_don]
+        b[orph] = g.permutation(cut_values(kind, "o", orph.size, g))
+        b[don] = g.uniform(TAU, 1.0, don.size).astype(np.float32)
+        if kind in ("two", "cluster"):  # m equal to the count of the lower group
+            low = np.full(orph.size, np.float32(0.25))
+            if kind == "cluster":  # the lower group differs in its low 12 bits
+                low = (low.view(np.int32) + g.integers(0, 4096, orph.size).astype(np.int32)
+                       ).view(np.float32)
+            b[orph] = np.where(np.arange(orph.size) < don.size, low, np.float32(0.375))
+    else:
+        don = don[: (6 * ret.size) // 10]
+        n_orph = max(1, don.size // 2 if kind in ("two", "cluster") else don.size // 7)
+        orph = orph[:n_orph]
+        b[don] = g.permutation(cut_values(kind, "d", don.size, g))
+        b[orph] = g.uniform(-1.0, TAU - 0.01, orph.size).astype(np.float32)
+        if kind in ("two", "cluster"):  # donors go in descending order: the higher group
+            high = np.full(don.size, np.float32(0.875))
+            if kind == "cluster":
+                high = (high.view(np.int32) + g.integers(0, 4096, don.size).astype(np.int32)
+                        ).view(np.float32)
+            b[don] = np.where(np.arange(don.size) < orph.size, high, np.float32(0.75))
+    return b, s0, B
+
+
+@pytest.mark.parametrize("n", [3000, 9000, 30000, 40000],
+                         ids=["short", "reg16", "reg32", "streaming"])
+def test_selection_edges_vs_oracle(n):
+    import torch
+    g = np.random.default_rng(n)
+    cases = [(kind, side) for kind in KINDS for side in ("o", "d")]
+    H = len(cases)
+    cu = np.array([0, n], np.int64)
+    b = np.zeros((H, n), np.float32)
+    s0 = np.zeros((H, n), np.uint8)
+    budget = None
+    for h, (kind, side) in enumerate(cases):
+        b[h], s0[h], budget = make_problem(n, kind, side, g)
+    out = binding.repair_from_scores(torch.from_numpy(b).cuda(), mask_to_device(s0), [budget],
+                                     TAU, N_SINK, N_RECENT, cu)
+    s1 = host(out["s1"])
+    st = host(out["stats"]).reshape(H, 4)
+    for h, (kind, side) in enumerate(cases):
+        r = oracle.repair(b[h].astype(np.float64), s0[h], TAU, N_SINK, N_RECENT)
+        assert r["m"] > 0, (kind, side)
+        assert (r["n_orphan"] > r["m"]) == (side == "o"), (kind, side)
+        assert np.array_equal(s1[h], r["s1"]), (kind, side)
+        assert st[h].tolist() == [r["n_orphan"], r["n_donor"], r["m"], 0], (kind, side)
