@@ -53,6 +53,61 @@ __device__ inline void hist_add(bool mem, int bin, int* s_hist) {
   if (mem && !peer) atomicAdd(&s_hist[bin], 1);
 }
 
+// One wave's part of a digit pass over BINS bins (call from one whole wave): the bin that
+// holds the rank-th smallest member (1-based), the members in lower bins and the members in
+// that bin go to s_pick[0..2].  Lane l sums bins BINS/64 l .. BINS/64 (l + 1) - 1; the lane
+// whose range holds the rank-th member walks its bins.
+template <int BINS = kSelBins>
+__device__ inline void wave_pick_bin(const int* hist, int rank, int* s_pick) {
+  constexpr int BPL = BINS / 64;
+  static_assert(BPL % 4 == 0, "whole 16-byte reads per lane");
+  const int lane = threadIdx.x & 63;
+  int hb[BPL];
+  int sum = 0;
+#pragma unroll
+  for (int j = 0; j < BPL / 4; ++j) {
+    const int4 h4 = *reinterpret_cast<const int4*>(&hist[BPL * lane + 4 * j]);
+    hb[4 * j + 0] = h4.x;
+    hb[4 * j + 1] = h4.y;
+    hb[4 * j + 2] = h4.z;
+    hb[4 * j + 3] = h4.w;
+    sum += h4.x + h4.y + h4.z + h4.w;
+  }
+  int inc = sum;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(inc, off);
+    if (lane >= off) inc += y;
+  }
+  int before = inc - sum;
+  if (before < rank && rank <= inc) {
+    int bin = -1, c = 0;
+#pragma unroll
+    for (int e = 0; e < BPL; ++e) {
+      if (bin < 0) {
+        if (rank <= before + hb[e]) {
+          bin = BPL * lane + e;
+          c = hb[e];
+        } else {
+          before += hb[e];
+        }
+      }
+    }
+    s_pick[0] = bin;
+    s_pick[1] = before;
+    s_pick[2] = c;
+  }
+}
+
+// Zero BINS bins (call from one whole wave).
+template <int BINS = kSelBins>
+__device__ inline void wave_clear_bins(int* hist) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < BINS / 256; ++j)
+    *reinterpret_cast<int4*>(&hist[BINS / 64 * lane + 4 * j]) = make_int4(0, 0, 0, 0);
+}
+
 // Among the members of [0, len) (member(t, key) returns true and sets key), the rank-th
 // smallest key (1-based rank, 1 <= rank <= number of members).  Returns that key; take_eq
 // receives how many members equal to it are needed so that exactly `rank` are taken when
