@@ -331,7 +331,7 @@ __global__ __launch_bounds__(NT, 8) void repair_short_kernel(RepairArgs a) {
   __syncthreads();
   uint64_t tot = 0;
 #pragma unroll
-  for (int k = 0; k < NW; ++k) tot += s_red[k];
+  for (int w = 0; w < NW; ++w) tot += s_red[w];
   const int tot_ret = (int)(tot & 0xFFFFu), tot_o = (int)((tot >> 16) & 0xFFFFu);
   const int tot_d = (int)((tot >> 32) & 0xFFFFu);
   const bool tot_bad = ((tot >> 48) & 0xFFFFu) != 0;
