@@ -1,7 +1,8 @@
 // Block-wide building blocks of the per-problem selection kernels (repair, scorer eviction):
-// an exclusive scan and an MSB-first radix select over 32-bit keys with 11/11/10-bit digits
-// (three passes over the data, LDS histograms of 2048 bins).  NT threads per block: 1024 for
-// long sequences, 256 when every sequence is short.
+// an exclusive scan, histogram adds, one wave's pick of a digit's bin and two MSB-first radix
+// selects over 32-bit keys (fixed 11/11/10-bit digits; or digits below the leading bits all
+// keys share, with an early stop), LDS histograms of up to 2048 bins.  NT threads per block:
+// 1024 for long sequences, 256 when every sequence is short.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -114,7 +115,9 @@ __device__ inline void wave_clear_bins(int* hist) {
 // every member below it is taken, and eq_total (if non-null) how many members equal it.
 // Workspace: s_hist[kSelBins], s_wave[NT / 64], s_pick[3].  Every thread of the block must
 // call it.
-// Digits: three passes of 11/11/10 bits over kSelBins = 2048 bins.
+// Digits: three passes of 11/11/10 bits over kSelBins = 2048 bins, every thread scanning two
+// bins (the streaming repair pass of sequences over 32768 tokens: measured faster there than
+// block_select_below, whose one-wave pick costs more per pass when all three passes run).
 struct SelDigits {
   static constexpr int PASSES = 3, BINS = kSelBins;
   static __device__ constexpr int shift(int p) { return p == 0 ? 21 : (p == 1 ? 10 : 0); }
@@ -173,6 +176,73 @@ __device__ inline uint32_t block_select(int len, int rank, Member member, int* s
     __syncthreads();
   }
   take_eq = kk;
+  return prefix;
+}
+
+// Among the members of [0, len) (member(t, key) returns true and sets key; n_members of them,
+// their keys' AND kand and OR kor), the rank-th smallest key (1-based, 1 <= rank <
+// n_members): MSB-first digits of up to DBITS bits below the leading bits every member key
+// shares, over 2^DBITS LDS bins, each pass reading the members afresh (8 slabs of NT tokens
+// per round, their loads in flight together); two barriers per pass, one wave picking the
+// bin while another clears the other histogram; the passes stop once the rank-th key's bucket
+// is taken whole.  Returns the cut key; take_eq receives how many members equal to it are
+// taken and eq_total how many there are (take_eq == eq_total: every member up to the cut is
+// taken).  s_hist: two histograms of 2^DBITS ints, the first zero and visible to every thread
+// on entry.  Every thread of the block must call it.
+template <int NT, int DBITS, class Member>
+__device__ inline uint32_t block_select_below(int len, int rank, int n_members, uint32_t kand,
+                                              uint32_t kor, Member member, int (*s_hist)[1 << DBITS],
+                                              int* s_pick, int& take_eq, int& eq_total) {
+  constexpr int BINS = 1 << DBITS;
+  constexpr int R = 8;  // slabs per round
+  static_assert(NT >= 128, "one wave picks while another clears");
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const uint32_t diff = kand ^ kor;
+  int hi = diff ? 32 - __clz(diff) : 0;
+  uint32_t mask = hi >= 32 ? 0u : (~0u << hi);
+  uint32_t prefix = kand & mask;
+  int kk = rank, cnt = n_members, buf = 0;
+#pragma unroll 1
+  while (hi > 0 && kk < cnt) {
+    const int shift = hi > DBITS ? hi - DBITS : 0;
+    const uint32_t dmask = (1u << (hi - shift)) - 1u;
+    // uniform trip count over the block, so that every lane of a wave takes part in the
+    // ballots of hist_add
+#pragma unroll 1
+    for (int t0 = 0; t0 < len; t0 += R * NT) {
+      uint32_t key[R];
+      bool mem[R];
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const int t = t0 + u * NT + tid;
+        key[u] = 0u;
+        mem[u] = t < len && member(t, key[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < R; ++u)
+        hist_add(mem[u] && (key[u] & mask) == prefix, (int)((key[u] >> shift) & dmask),
+                 s_hist[buf]);
+    }
+    __syncthreads();
+    if (wave == 0) wave_pick_bin<BINS>(s_hist[buf], kk, s_pick);
+    else if (wave == 1) wave_clear_bins<BINS>(s_hist[buf ^ 1]);
+    __syncthreads();
+    kk -= s_pick[1];
+    prefix |= (uint32_t)s_pick[0] << shift;
+    mask |= dmask << shift;
+    cnt = s_pick[2];
+    hi = shift;
+    buf ^= 1;
+  }
+  eq_total = cnt;
+  if (kk == cnt) {
+    // every member sharing bits [hi, 32) with the rank-th key is taken: cut at the largest
+    // key with those bits
+    take_eq = cnt;
+    return prefix | ~mask;
+  }
+  take_eq = kk;  // hi == 0: the rank-th key itself; cnt members equal it
   return prefix;
 }
 

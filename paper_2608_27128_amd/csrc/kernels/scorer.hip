@@ -10,7 +10,7 @@
 // are kept.  Sequences of up to 32768 tokens keep their keys in LDS (evict_lds_kernel: one
 // round of loads, digits below the leading bits all keys share, an early stop, the members
 // equal to the cut ranked with one count per slab and wave); longer ones stream the counts
-// from HBM on every pass (evict_kernel: 11/11/10-bit digits, ranking slab by slab).
+// from HBM on every pass (evict_kernel: the same digits, ranking slab by slab).
 //
 // Policy selection (FROM_SCORES): the same with a caller's fp32 scores.  The key is 0 for
 // protected positions and otherwise the score's bits mapped to an order-reversing integer
@@ -38,17 +38,21 @@ __device__ inline uint32_t score_key(float f) {
   return ~u;
 }
 
-// CAP > 0: the problem's counts (keys of its scores) are copied to LDS in the first pass
-// (sequences of at most CAP tokens), so HBM is read once; CAP = 0: every pass reads global
-// memory.  (Launched with CAP = 0 only: evict_lds_kernel takes the shorter sequences.)
-template <int NT, int CAP, bool FROM_SCORES>
+// Sequences of any length: every pass streams the counts (scores) from HBM, 8 slabs of NT
+// tokens per thread and round with the round's loads in flight together.  The first pass
+// writes the Eq. 3 scores and takes the AND and OR of the keys; the selection's digits start
+// below the leading bits they share and stop once the cut's bucket is taken whole; the keys
+// equal to the cut are ranked slab by slab (two barriers per slab) only when some of them
+// must be left out.
+template <int NT, bool FROM_SCORES>
 __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
-  static_assert(CAP % NT == 0, "the cache holds whole slabs");
-  __shared__ int s_wave[NT / 64];
-  __shared__ int s_hist[kSelBins];
+  constexpr int NW = NT / 64;
+  constexpr int R = 8;  // slabs per round
+  __shared__ int s_wave[NW];
+  __shared__ uint32_t s_bits[NW][2];
+  __shared__ int s_nan[NW];
+  __shared__ int s_hist[2][kSelBins];  // digit histograms, used in turn
   __shared__ int s_pick[3];
-  __shared__ int s_nan;
-  __shared__ uint32_t s_c[CAP > 0 ? CAP : 1];
 
   const int q = blockIdx.x;
   const int h = q / a.n_seqs;
@@ -65,56 +69,84 @@ __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
   const int wave = tid >> 6;
   const int budget = si.budget < len ? si.budget : len;
   const float inv_n = len > 0 ? 1.0f / (float)len : 0.0f;
-  // unprotected key: count + 1, or the score's key
-  auto free_key = [&](int t) -> uint32_t {
-    if constexpr (CAP > 0) return s_c[t];
-    else if constexpr (FROM_SCORES) return score_key(psc[t]);
+  // protected positions take the key 0; the others count + 1, or the score's key
+  auto key_of = [&](int t) -> uint32_t {
+    if (t < a.n_sink || t >= rec0) return 0u;
+    if constexpr (FROM_SCORES) return score_key(psc[t]);
     else return (uint32_t)cnt[t] + 1u;
   };
-  auto key_of = [&](int t) -> uint32_t {
-    return (t < a.n_sink || t >= rec0) ? 0u : free_key(t);
-  };
 
-  // ---- pass 1: the LDS copy, the Eq. 3 scores, the NaN count of the policy scores ----
-  if constexpr (FROM_SCORES) {
-    if (tid == 0) s_nan = 0;
-    __syncthreads();
-    int nan = 0;
-    for (int t = tid; t < len; t += NT) {
-      const float f = psc[t];
-      nan += (f != f) ? 1 : 0;
-      if constexpr (CAP > 0) s_c[t] = score_key(f);
+  for (int i = tid; i < kSelBins; i += NT) s_hist[0][i] = 0;  // visible after the next barrier
+
+  // ---- pass 1: the AND and OR of the keys, the Eq. 3 scores, the NaN count of the policy
+  // scores ----
+  uint32_t kand = ~0u, kor = 0u;
+  int nan = 0;
+#pragma unroll 1
+  for (int t0 = 0; t0 < len; t0 += R * NT) {
+    float f[R];
+    int32_t c[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int t = t0 + u * NT + tid;
+      if constexpr (FROM_SCORES) f[u] = t < len ? psc[t] : 0.0f;
+      else c[u] = t < len ? cnt[t] : 0;
     }
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) nan += __shfl_xor(nan, off);
-    if (lane == 0 && nan) atomicAdd(&s_nan, nan);
-  } else if (CAP > 0 || a.scores) {
-    for (int t = tid; t < len; t += NT) {
-      const int32_t c = cnt[t];
-      if constexpr (CAP > 0) s_c[t] = (uint32_t)c + 1u;
-      if (a.scores) a.scores[base + t] = -(float)c * inv_n;
+    for (int u = 0; u < R; ++u) {
+      const int t = t0 + u * NT + tid;
+      if (t < len) {
+        const bool pr = t < a.n_sink || t >= rec0;
+        uint32_t k;
+        if constexpr (FROM_SCORES) {
+          nan += (f[u] != f[u]) ? 1 : 0;
+          k = pr ? 0u : score_key(f[u]);
+        } else {
+          k = pr ? 0u : (uint32_t)c[u] + 1u;
+          if (a.scores) a.scores[base + t] = -(float)c[u] * inv_n;
+        }
+        kand &= k;
+        kor |= k;
+      }
     }
   }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    kand &= __shfl_xor(kand, off);
+    kor |= __shfl_xor(kor, off);
+    nan += __shfl_xor(nan, off);
+  }
+  if (lane == 0) {
+    s_bits[wave][0] = kand;
+    s_bits[wave][1] = kor;
+    s_nan[wave] = nan;
+  }
   __syncthreads();
+  int n_nan = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    kand &= s_bits[w][0];
+    kor |= s_bits[w][1];
+    n_nan += s_nan[w];
+  }
 
   // ---- radix select of the budget-th smallest key ----
   uint32_t key_cut = 0u;
   int take_eq = 0, total_eq = 0;
   const bool cut = budget > 0 && budget < len;
   if (cut) {
-    key_cut = block_select<NT>(
-        len, budget,
+    key_cut = block_select_below<NT, 11>(
+        len, budget, len, kand, kor,
         [&](int t, uint32_t& key) {
           key = key_of(t);
           return true;
         },
-        s_hist, s_wave, s_pick, take_eq);
-    // the last digit's histogram still holds the number of keys equal to the cut
-    total_eq = s_hist[key_cut & 1023u];
+        s_hist, s_pick, take_eq, total_eq);
   }
+  const bool rank_eq = cut && take_eq < total_eq;
 
-  // ---- final pass, slab by slab: the last (policy scores: the first) take_eq keys equal to
-  // the cut are kept ----
+  // ---- final pass: keys below the cut are kept, and of those equal to it the last take_eq
+  // (policy scores: the first), ranked slab by slab when some of them must be left out ----
   const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
   int eq_before = 0;
   for (int t0 = 0; t0 < len; t0 += NT) {
@@ -122,21 +154,24 @@ __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
     const bool valid = t < len;
     const uint32_t key = valid ? key_of(t) : 0u;
     const bool eq = cut && valid && key == key_cut;
-    const uint64_t bal = __ballot(eq);
-    if (lane == 0) s_wave[wave] = __popcll(bal);
-    __syncthreads();
-    int rank = eq_before + __popcll(bal & below);
+    int rank = 0;
+    if (rank_eq) {
+      const uint64_t bal = __ballot(eq);
+      if (lane == 0) s_wave[wave] = __popcll(bal);
+      __syncthreads();
+      rank = eq_before + __popcll(bal & below);
 #pragma unroll
-    for (int k = 0; k < NT / 64; ++k) {
-      const int c = s_wave[k];
-      rank += k < wave ? c : 0;
-      eq_before += c;
+      for (int w = 0; w < NW; ++w) {
+        const int c = s_wave[w];
+        rank += w < wave ? c : 0;
+        eq_before += c;
+      }
+      __syncthreads();
     }
-    __syncthreads();
     uint8_t keep;
     if (!cut) keep = budget > 0 ? 1 : 0;
     else if (key < key_cut) keep = 1;
-    else if (key == key_cut) keep = (FROM_SCORES ? rank < take_eq : rank >= total_eq - take_eq) ? 1 : 0;
+    else if (eq) keep = !rank_eq || (FROM_SCORES ? rank < take_eq : rank >= total_eq - take_eq);
     else keep = 0;
     if (valid) out[t] = keep;
   }
@@ -144,7 +179,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(EvictArgs a) {
     int32_t* st = a.stats + 4 * (int64_t)q;
     st[0] = budget;
     if constexpr (FROM_SCORES) {
-      st[1] = s_nan;
+      st[1] = n_nan;
       st[2] = 0;
     } else {
       st[1] = cut ? (key_cut == 0u ? -1 : (int32_t)(key_cut - 1u)) : -1;
@@ -411,7 +446,7 @@ void launch_evict_mode(const EvictArgs& a, hipStream_t st) {
   else if (a.max_len <= 32768)
     hipLaunchKernelGGL((evict_lds_kernel<1024, 32768, FROM_SCORES>), grid, dim3(1024), 0, st, a);
   else
-    hipLaunchKernelGGL((evict_kernel<1024, 0, FROM_SCORES>), grid, dim3(1024), 0, st, a);
+    hipLaunchKernelGGL((evict_kernel<1024, FROM_SCORES>), grid, dim3(1024), 0, st, a);
 }
 
 int launch_evict(const EvictArgs& a, void* stream) {
