@@ -267,6 +267,7 @@ def test_repair_budget_mismatch_and_aliasing():
 @pytest.mark.parametrize("want_all", [True, False], ids=["both", "retained_only"])
 @pytest.mark.parametrize("d,dtype,tau,w", [(64, "bf16", 0.9, 32), (128, "bf16", 0.85, 32),
                                            (128, "bf16", 0.95, 64), (64, "f32", 0.9, 16),
+                                           (128, "bf16", 0.97, 128), (64, "bf16", 0.97, 64),
                                            (128, "f32", 0.9, 32),
                                            (128, "bf16", 1.5, 32), (64, "bf16", -1.5, 32)])
 def test_repair_vs_oracle(d, dtype, tau, w, want_all):
