@@ -16,8 +16,8 @@
 //    once, in one round of loads, into 16 or 32 slots per thread (the keys of b in registers
 //    up to 16384 tokens, in LDS beyond); digit passes of up to 11 bits over 2048 LDS bins,
 //    below the leading bits the cut side's keys share, read the slots.
-//  * Longer sequences (repair_kernel, 1024 threads): the same digits, every pass streaming
-//    b and S0 from global memory.
+//  * Longer sequences (repair_kernel, 1024 threads): fixed 11/11/10-bit digits over the whole
+//    key, every pass streaming b and S0 from global memory.
 #include <hip/hip_runtime.h>
 
 #include "../twinkv_internal.h"

@@ -6,11 +6,12 @@
 // and the `budget` highest scores are retained; equal scores go to the later position first.
 // Ranking by the key  0 for protected positions, r_i + 1 otherwise  (ascending) gives the
 // same order.  The budget-th smallest key is found by an MSB-first radix select (LDS
-// histograms of 2048 bins, 1024 or 256 threads), and the last members equal to it by position
-// are kept.  Sequences of up to 32768 tokens keep their keys in LDS (evict_lds_kernel: one
+// histograms of 2048 bins with 1024 threads, of 256 bins with 256 threads), and the last
+// members equal to it by position are kept.  Sequences of up to 32768 tokens keep their keys in LDS (evict_lds_kernel: one
 // round of loads, digits below the leading bits all keys share, an early stop, the members
 // equal to the cut ranked with one count per slab and wave); longer ones stream the counts
-// from HBM on every pass (evict_kernel: the same digits, ranking slab by slab).
+// from HBM on every pass (evict_kernel: 11-bit digits below the shared bits, ranking slab by
+// slab).
 //
 // Policy selection (FROM_SCORES): the same with a caller's fp32 scores.  The key is 0 for
 // protected positions and otherwise the score's bits mapped to an order-reversing integer
