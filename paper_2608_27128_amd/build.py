@@ -78,11 +78,31 @@ def _build_one(lib: str, objdir: str, extra: list, verbose: bool) -> str:
     return lib
 
 
+CLIENT_SRC = os.path.join(HERE, "examples", "repair_client.c")
+CLIENT = os.path.join(BUILD, "repair_client")
+
+
+def _build_client(verbose: bool) -> str:
+    """The plain C example client (examples/repair_client.c), linked against libtwinkv.so
+    (found next to the _build folder at run time) and the HIP runtime."""
+    cc = shutil.which("gcc") or "gcc"
+    tmp = CLIENT + ".tmp"
+    _run([cc, "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+          f"-I{os.path.join(ROCM, 'include')}", f"-I{os.path.join(ROOT, 'include')}",
+          CLIENT_SRC, "-o", tmp, f"-L{HERE}", "-ltwinkv", f"-L{os.path.join(ROCM, 'lib')}",
+          "-lamdhip64", "-Wl,-rpath,$ORIGIN/..", f"-Wl,-rpath,{os.path.join(ROCM, 'lib')}"],
+         verbose)
+    os.replace(tmp, CLIENT)
+    return CLIENT
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source and link libtwinkv.so, plus libtwinkv_debug.so (the LDS-poisoning
-    build the tests compare against it, -DTWINKV_DEBUG); returns the library path."""
+    build the tests compare against it, -DTWINKV_DEBUG) and the C example client; returns the
+    library path."""
     _build_one(LIB, BUILD, [], verbose)
     _build_one(DEBUG_LIB, os.path.join(BUILD, "debug"), ["-DTWINKV_DEBUG"], verbose)
+    _build_client(verbose)
     return LIB
 
 
