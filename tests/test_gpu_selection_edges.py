@@ -5,7 +5,8 @@ at the end of the first (whose scores differ in their low 12 bits, so the bucket
 key holds many distinct keys when the selection stops early), and that span both signs.  The
 selection skips the leading bits the cut side's keys share and stops once the m-th key's
 bucket is taken whole; every case must still give the oracle's S1 and counts bit for bit, for
-each kernel (up to 4096 tokens, up to 16384, up to 32768, longer)."""
+each kernel (up to 4096 tokens, up to 16384, up to 32768, longer).  The degenerate cases, where
+m = 0 and nothing may move, are covered on every kernel too."""
 import numpy as np
 import pytest
 
@@ -104,3 +105,40 @@ def test_selection_edges_vs_oracle(n):
         assert (r["n_orphan"] > r["m"]) == (side == "o"), (kind, side)
         assert np.array_equal(s1[h], r["s1"]), (kind, side)
         assert st[h].tolist() == [r["n_orphan"], r["n_donor"], r["m"], 0], (kind, side)
+
+
+def run_vs_oracle(b, s0, budget, tau, n_sink, n_recent):
+    import torch
+    H, n = b.shape
+    out = binding.repair_from_scores(torch.from_numpy(b).cuda(), mask_to_device(s0), [budget],
+                                     tau, n_sink, n_recent, np.array([0, n], np.int64))
+    s1, st = host(out["s1"]), host(out["stats"]).reshape(H, 4)
+    for h in range(H):
+        r = oracle.repair(b[h].astype(np.float64), s0[h], tau, n_sink, n_recent)
+        assert np.array_equal(s1[h], r["s1"]), h
+        assert st[h].tolist() == [r["n_orphan"], r["n_donor"], r["m"], 0], h
+    return s1, st
+
+
+@pytest.mark.parametrize("n", [3000, 9000, 30000, 40000],
+                         ids=["short", "reg16", "reg32", "streaming"])
+def test_degenerate_sets_vs_oracle(n):
+    """Cases where nothing may move (Sec. 3.4: m = min(|O|, |D|) = 0): S0 empty (budget 0, no
+    donors), S0 holding every position (no orphans), every position protected (no donors),
+    and tau above or below every score; on each K3 kernel S1 must equal S0 and the counts
+    the oracle's."""
+    g = np.random.default_rng(n + 1)
+    H = 3
+    b = g.uniform(-1.0, 1.0, (H, n)).astype(np.float32)
+    half = np.zeros((H, n), np.uint8)
+    for h in range(H):
+        half[h, g.permutation(n)[: n // 2]] = 1
+    s0_none = np.zeros((H, n), np.uint8)
+    s0_all = np.ones((H, n), np.uint8)
+    cases = [(s0_none, 0, 0.5, N_SINK, N_RECENT), (s0_all, n, 0.5, N_SINK, N_RECENT),
+             (half, n // 2, 0.5, n // 2, n - n // 2), (half, n // 2, 1.5, N_SINK, N_RECENT),
+             (half, n // 2, -1.5, N_SINK, N_RECENT)]
+    for s0, budget, tau, ns, nr in cases:
+        s1, st = run_vs_oracle(b, s0, budget, tau, ns, nr)
+        assert np.array_equal(s1, s0), (budget, tau, ns, nr)
+        assert np.all(st[:, 2] == 0), (budget, tau, ns, nr)
