@@ -228,10 +228,19 @@ def _mask(x, n_heads, T, device, name):
     return x.contiguous()
 
 
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
 def _workspace(workspace, nbytes: int, dev):
+    """The caller's workspace when it is large enough (a contiguous tensor on the call's
+    device; its byte count is what is compared), else a fresh uint8 buffer of nbytes."""
     torch = _torch()
-    if workspace is not None and workspace.numel() >= nbytes:
-        return workspace
+    if workspace is not None:
+        if workspace.device != dev or not workspace.is_contiguous():
+            raise ValueError(f"workspace must be a contiguous tensor on {dev}")
+        if _nbytes(workspace) >= nbytes:
+            return workspace
     return torch.empty((nbytes,), dtype=torch.uint8, device=dev)
 
 
@@ -259,7 +268,7 @@ def nn_scores(keys, retained=None, w: int = 32, cu_seqlens=None, *, want_arg: bo
         keys.data_ptr(), dt, d, H, len(cu) - 1, _i64_array(cu), keys.stride(0), keys.stride(1),
         _ptr(ret), int(w), _ptr(out["best_all"]), _ptr(out["arg_all"]),
         _ptr(out.get("best_ret")), _ptr(out.get("arg_ret")), _ptr(out["status"]),
-        ws.data_ptr(), ws.numel(), _stream(dev))
+        ws.data_ptr(), _nbytes(ws), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_nn_scores", rc)
     return {k: v for k, v in out.items() if v is not None}
@@ -308,7 +317,7 @@ def nn_scores_levels(keys, level, n_levels: int, w: int = 32, cu_seqlens=None, *
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         lv.data_ptr(), int(n_levels), int(w), _ptr(out.get("best_all")), _ptr(out.get("arg_all")),
         out["best_lvl"].data_ptr(), _ptr(out.get("arg_lvl")), _ptr(out["status"]),
-        ws.data_ptr(), ws.numel(), _stream(dev))
+        ws.data_ptr(), _nbytes(ws), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_nn_scores_levels", rc)
     return {k: v for k, v in out.items() if v is not None}
@@ -368,7 +377,7 @@ def repair(keys, retained, budget, tau: float, w: int = 32, n_sink: int = 4, n_r
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         ret.data_ptr(), out["s1"].data_ptr(), _i64_array(bud), float(tau), int(w), int(n_sink),
         int(n_recent), out["stats"].data_ptr(), _ptr(out.get("best_all")), _ptr(out.get("arg_all")),
-        _ptr(out.get("best_ret")), _ptr(out.get("arg_ret")), ws.data_ptr(), ws.numel(), _stream(dev))
+        _ptr(out.get("best_ret")), _ptr(out.get("arg_ret")), ws.data_ptr(), _nbytes(ws), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_repair", rc)
     return {k: v for k, v in out.items() if v is not None}
@@ -398,7 +407,7 @@ def repair_from_scores(b, retained, budget, tau: float, n_sink: int = 4, n_recen
     ws = _workspace(None, workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu), dev)
     rc = lib().twinkv_repair_from_scores(
         b.data_ptr(), ret.data_ptr(), s1.data_ptr(), H, n_seqs, _i64_array(cu), _i64_array(bud),
-        float(tau), int(n_sink), int(n_recent), stats.data_ptr(), ws.data_ptr(), ws.numel(),
+        float(tau), int(n_sink), int(n_recent), stats.data_ptr(), ws.data_ptr(), _nbytes(ws),
         _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_repair_from_scores", rc)
@@ -452,7 +461,7 @@ def twin_counts(keys, tau: float, w: int = 32, cu_seqlens=None, *, workspace=Non
     ws = _workspace(workspace, workspace_bytes(OP_TWIN_COUNTS, dt, d, H, cu), dev)
     rc = lib().twinkv_twin_counts(
         keys.data_ptr(), dt, d, H, len(cu) - 1, _i64_array(cu), keys.stride(0), keys.stride(1),
-        float(tau), int(w), counts.data_ptr(), status.data_ptr(), ws.data_ptr(), ws.numel(),
+        float(tau), int(w), counts.data_ptr(), status.data_ptr(), ws.data_ptr(), _nbytes(ws),
         _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_twin_counts", rc)
@@ -494,7 +503,7 @@ def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         _i64_array(bud), float(tau), int(w), int(n_sink), int(n_recent),
         out["retained"].data_ptr(), out["counts"].data_ptr(), _ptr(out["scores"]),
-        out["stats"].data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev))
+        out["stats"].data_ptr(), ws.data_ptr(), _nbytes(ws), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_score_evict", rc)
     return {k: v for k, v in out.items() if v is not None}
@@ -527,7 +536,7 @@ def select_topk(scores, budget, n_sink: int = 4, n_recent: int = 64, cu_seqlens=
     rc = lib().twinkv_select_topk(
         scores.data_ptr(), H, n_seqs, _i64_array(cu), _i64_array(bud), int(n_sink),
         int(n_recent), out["retained"].data_ptr(), _ptr(out["stats"]), ws.data_ptr(),
-        ws.numel(), _stream(dev))
+        _nbytes(ws), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_select_topk", rc)
     return out
@@ -551,7 +560,7 @@ def prevalence(best_all, taus, cu_seqlens=None) -> "torch.Tensor":
     rc = lib().twinkv_prevalence(
         best_all.data_ptr(), H, n_seqs, _i64_array(cu),
         tv.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(tv), out.data_ptr(),
-        ws.data_ptr(), ws.numel(), _stream(dev))
+        ws.data_ptr(), _nbytes(ws), _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_prevalence", rc)
     return out
@@ -609,7 +618,7 @@ def compact(keys, retained, capacity, values=None, cu_seqlens=None, *, want_pos:
     rc = lib().twinkv_compact(
         keys.data_ptr(), _ptr(values), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0),
         keys.stride(1), vs[0], vs[1], ret.data_ptr(), _i64_array(cap), out["keys"].data_ptr(),
-        _ptr(out["values"]), _ptr(out["pos"]), out["stats"].data_ptr(), ws.data_ptr(), ws.numel(),
+        _ptr(out["values"]), _ptr(out["pos"]), out["stats"].data_ptr(), ws.data_ptr(), _nbytes(ws),
         _stream(dev))
     if rc != TWINKV_OK:
         raise TwinKVError("twinkv_compact", rc)

@@ -72,3 +72,24 @@ def test_repair_and_scores_ignore_workspace_contents(H, lens, d, dtype, w):
     c0 = binding.twin_counts(kt, sp.tau, w, cu, workspace=zero)
     c1 = binding.twin_counts(kt, sp.tau, w, cu, workspace=poison)
     same(c0, c1, ["counts"])
+
+
+def test_workspace_on_another_device_or_strided_is_refused():
+    """A workspace the kernels could not address as one device buffer (host memory, a strided
+    view) is refused before the call; one given as wider elements counts by bytes."""
+    import torch
+    batch = synth.make_batch(spec_of(2, [300, 41], 128, "bf16", 32, 7))
+    sp = batch.spec
+    kt, ret = to_device(batch.keys, "bf16"), mask_to_device(batch.retained)
+    cu = batch.cu_seqlens
+    nbytes = binding.workspace_bytes(binding.OP_REPAIR, 0, 128, 2, cu)
+    args = (kt, ret, batch.budget, sp.tau, sp.w, sp.n_sink, sp.n_recent, cu)
+    with pytest.raises(ValueError, match="workspace"):
+        binding.repair(*args, workspace=torch.zeros((nbytes,), dtype=torch.uint8))
+    with pytest.raises(ValueError, match="workspace"):
+        binding.repair(*args, workspace=torch.zeros((2 * nbytes,), dtype=torch.uint8,
+                                                    device="cuda")[::2])
+    ref = binding.repair(*args)
+    wide = torch.full(((nbytes + 3) // 4,), -1, dtype=torch.int32, device="cuda")
+    got = binding.repair(*args, workspace=wide)
+    same(ref, got, ["s1", "stats", "best_ret", "arg_ret", "best_all", "arg_all"])
