@@ -228,6 +228,16 @@ def _mask(x, n_heads, T, device, name):
     return x.contiguous()
 
 
+def _launch(dev, name: str, *args) -> None:
+    """Call the library entry point ``name`` with the tensors' device current: the library
+    enqueues on the given stream of the current device and keeps its per-device state there."""
+    torch = _torch()
+    with torch.cuda.device(dev):
+        rc = getattr(lib(), name)(*args)
+    if rc != TWINKV_OK:
+        raise TwinKVError(name, rc)
+
+
 def _nbytes(t) -> int:
     return t.numel() * t.element_size()
 
@@ -264,13 +274,11 @@ def nn_scores(keys, retained=None, w: int = 32, cu_seqlens=None, *, want_arg: bo
         out["best_ret"] = torch.empty((H, T), dtype=torch.float32, device=dev)
         out["arg_ret"] = torch.empty((H, T), dtype=torch.int32, device=dev) if want_arg else None
     ws = _workspace(workspace, workspace_bytes(OP_NN_SCORES, dt, d, H, cu), dev)
-    rc = lib().twinkv_nn_scores(
+    _launch(dev, "twinkv_nn_scores",
         keys.data_ptr(), dt, d, H, len(cu) - 1, _i64_array(cu), keys.stride(0), keys.stride(1),
         _ptr(ret), int(w), _ptr(out["best_all"]), _ptr(out["arg_all"]),
         _ptr(out.get("best_ret")), _ptr(out.get("arg_ret")), _ptr(out["status"]),
         ws.data_ptr(), _nbytes(ws), _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_nn_scores", rc)
     return {k: v for k, v in out.items() if v is not None}
 
 
@@ -313,13 +321,11 @@ def nn_scores_levels(keys, level, n_levels: int, w: int = 32, cu_seqlens=None, *
         out = _check_outputs(outputs, spec, "nn_scores_levels")
         want_all = out.get("best_all") is not None or out.get("arg_all") is not None
     ws = _workspace(workspace, levels_workspace_bytes(dt, d, H, cu, n_levels, want_all), dev)
-    rc = lib().twinkv_nn_scores_levels(
+    _launch(dev, "twinkv_nn_scores_levels",
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         lv.data_ptr(), int(n_levels), int(w), _ptr(out.get("best_all")), _ptr(out.get("arg_all")),
         out["best_lvl"].data_ptr(), _ptr(out.get("arg_lvl")), _ptr(out["status"]),
         ws.data_ptr(), _nbytes(ws), _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_nn_scores_levels", rc)
     return {k: v for k, v in out.items() if v is not None}
 
 
@@ -373,13 +379,11 @@ def repair(keys, retained, budget, tau: float, w: int = 32, n_sink: int = 4, n_r
             raise ValueError("out_mask must be a contiguous uint8 (n_heads, T) tensor")
         out["s1"] = out_mask
     ws = _workspace(workspace, workspace_bytes(OP_REPAIR, dt, d, H, cu), dev)
-    rc = lib().twinkv_repair(
+    _launch(dev, "twinkv_repair",
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         ret.data_ptr(), out["s1"].data_ptr(), _i64_array(bud), float(tau), int(w), int(n_sink),
         int(n_recent), out["stats"].data_ptr(), _ptr(out.get("best_all")), _ptr(out.get("arg_all")),
         _ptr(out.get("best_ret")), _ptr(out.get("arg_ret")), ws.data_ptr(), _nbytes(ws), _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_repair", rc)
     return {k: v for k, v in out.items() if v is not None}
 
 
@@ -405,12 +409,10 @@ def repair_from_scores(b, retained, budget, tau: float, n_sink: int = 4, n_recen
         s1 = torch.empty((H, T), dtype=torch.uint8, device=dev)
     stats = torch.empty((H * n_seqs, 4), dtype=torch.int32, device=dev)
     ws = _workspace(None, workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu), dev)
-    rc = lib().twinkv_repair_from_scores(
+    _launch(dev, "twinkv_repair_from_scores",
         b.data_ptr(), ret.data_ptr(), s1.data_ptr(), H, n_seqs, _i64_array(cu), _i64_array(bud),
         float(tau), int(n_sink), int(n_recent), stats.data_ptr(), ws.data_ptr(), _nbytes(ws),
         _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_repair_from_scores", rc)
     return {"s1": s1, "stats": stats}
 
 
@@ -439,12 +441,10 @@ def repair_from_scores_noalloc(b, retained, budget, tau: float, n_sink: int = 4,
         raise ValueError(f"retained must be a contiguous uint8 ({H}, {T}) tensor on {dev}")
     spec = {"s1": ((H, T), torch.uint8, dev, True), "stats": ((H * n_seqs, 4), torch.int32, dev, True)}
     out = _check_outputs(outputs, spec, "repair_from_scores_noalloc")
-    rc = lib().twinkv_repair_from_scores_noalloc(
+    _launch(dev, "twinkv_repair_from_scores_noalloc",
         b.data_ptr(), retained.data_ptr(), out["s1"].data_ptr(), H, n_seqs, _i64_array(cu),
         _i64_array(bud), float(tau), int(n_sink), int(n_recent), out["stats"].data_ptr(),
         _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_repair_from_scores_noalloc", rc)
     return out
 
 
@@ -459,12 +459,10 @@ def twin_counts(keys, tau: float, w: int = 32, cu_seqlens=None, *, workspace=Non
     counts = torch.empty((H, T), dtype=torch.int32, device=dev)
     status = torch.empty((H * (len(cu) - 1),), dtype=torch.int32, device=dev)
     ws = _workspace(workspace, workspace_bytes(OP_TWIN_COUNTS, dt, d, H, cu), dev)
-    rc = lib().twinkv_twin_counts(
+    _launch(dev, "twinkv_twin_counts",
         keys.data_ptr(), dt, d, H, len(cu) - 1, _i64_array(cu), keys.stride(0), keys.stride(1),
         float(tau), int(w), counts.data_ptr(), status.data_ptr(), ws.data_ptr(), _nbytes(ws),
         _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_twin_counts", rc)
     return {"counts": counts, "status": status}
 
 
@@ -499,13 +497,11 @@ def score_evict(keys, budget, tau: float, w: int = 32, n_sink: int = 4, n_recent
         out = _check_outputs(outputs, spec, "score_evict")
         out.setdefault("scores", None)
     ws = _workspace(workspace, workspace_bytes(OP_SCORE_EVICT, dt, d, H, cu), dev)
-    rc = lib().twinkv_score_evict(
+    _launch(dev, "twinkv_score_evict",
         keys.data_ptr(), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0), keys.stride(1),
         _i64_array(bud), float(tau), int(w), int(n_sink), int(n_recent),
         out["retained"].data_ptr(), out["counts"].data_ptr(), _ptr(out["scores"]),
         out["stats"].data_ptr(), ws.data_ptr(), _nbytes(ws), _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_score_evict", rc)
     return {k: v for k, v in out.items() if v is not None}
 
 
@@ -533,12 +529,10 @@ def select_topk(scores, budget, n_sink: int = 4, n_recent: int = 64, cu_seqlens=
                 "stats": ((H * n_seqs, 4), torch.int32, dev, True)}
         out = _check_outputs(outputs, spec, "select_topk")
     ws = _workspace(workspace, workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu), dev)
-    rc = lib().twinkv_select_topk(
+    _launch(dev, "twinkv_select_topk",
         scores.data_ptr(), H, n_seqs, _i64_array(cu), _i64_array(bud), int(n_sink),
         int(n_recent), out["retained"].data_ptr(), _ptr(out["stats"]), ws.data_ptr(),
         _nbytes(ws), _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_select_topk", rc)
     return out
 
 
@@ -557,12 +551,10 @@ def prevalence(best_all, taus, cu_seqlens=None) -> "torch.Tensor":
     dev = best_all.device
     out = torch.empty((H * n_seqs, len(tv)), dtype=torch.int32, device=dev)
     ws = _workspace(None, workspace_bytes(OP_REPAIR_FROM_SCORES, 0, 64, H, cu), dev)
-    rc = lib().twinkv_prevalence(
+    _launch(dev, "twinkv_prevalence",
         best_all.data_ptr(), H, n_seqs, _i64_array(cu),
         tv.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(tv), out.data_ptr(),
         ws.data_ptr(), _nbytes(ws), _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_prevalence", rc)
     return out
 
 
@@ -615,11 +607,9 @@ def compact(keys, retained, capacity, values=None, cu_seqlens=None, *, want_pos:
             out["values"] = None
     ws = _workspace(workspace, workspace_bytes(OP_COMPACT, dt, d, H, cu), dev)
     vs = (values.stride(0), values.stride(1)) if values is not None else (0, 0)
-    rc = lib().twinkv_compact(
+    _launch(dev, "twinkv_compact",
         keys.data_ptr(), _ptr(values), dt, d, H, n_seqs, _i64_array(cu), keys.stride(0),
         keys.stride(1), vs[0], vs[1], ret.data_ptr(), _i64_array(cap), out["keys"].data_ptr(),
         _ptr(out["values"]), _ptr(out["pos"]), out["stats"].data_ptr(), ws.data_ptr(), _nbytes(ws),
         _stream(dev))
-    if rc != TWINKV_OK:
-        raise TwinKVError("twinkv_compact", rc)
     return {k: v for k, v in out.items() if v is not None}
