@@ -341,6 +341,61 @@ def _brute_counts(K, tau, w):
     return out
 
 
+def _brute_best(K, member, w):
+    """Pure-Python Eq. 1 maximised over j with |i-j| > w (Sec. 3.2's window) and, when member
+    is given, j in that set (Eq. 4): its own norms and dot products, a zero key at similarity
+    0 with everything.  Per row: (best, smallest maximising j, best of the other values, the
+    similarity of every candidate j), with (-1, -1, -inf, {}) where no j qualifies."""
+    import math
+    n = len(K)
+    norms = [math.sqrt(math.fsum(float(x) * float(x) for x in k)) for k in K]
+    out = []
+    for i in range(n):
+        cand = []
+        for j in range(n):
+            if abs(i - j) <= w or (member is not None and not member[j]):
+                continue
+            if norms[i] == 0.0 or norms[j] == 0.0:
+                s = 0.0
+            else:
+                s = math.fsum(float(a) * float(b) for a, b in zip(K[i], K[j])) / (norms[i] * norms[j])
+            cand.append((s, j))
+        if not cand:
+            out.append((-1.0, -1, -math.inf, {}))
+            continue
+        best = max(s for s, _ in cand)
+        arg = min(j for s, j in cand if s == best)
+        rest = [s for s, _ in cand if s != best]
+        out.append((best, arg, max(rest) if rest else -math.inf, dict((j, s) for s, j in cand)))
+    return out
+
+
+def pin_nn_scores_brute_force(o):
+    """Eq. 1 and Eq. 4 against a pure-Python brute force on tiny inputs: random keys with
+    exact duplicates (ties go to the smallest position), zero keys, windows from 0 to past
+    the sequence, and retained sets from empty to full."""
+    rng = np.random.default_rng(21)
+    for trial in range(12):
+        n, d = int(rng.integers(2, 17)), int(rng.integers(1, 6))
+        w = int(rng.choice([0, 1, 2, 3, n]))
+        K = rng.standard_normal((n, d)).astype(np.float32)
+        for _ in range(int(rng.integers(0, 3))):   # exact duplicates: exact ties
+            a, b = rng.choice(n, 2, replace=False)
+            K[b] = K[a]
+        if trial % 3 == 0:
+            K[rng.integers(n)] = 0.0
+        member = (rng.random(n) < [0.0, 0.5, 1.0][trial % 3]).astype(np.uint8)
+        r = o.nn_scores(K, "f32", member, w)
+        for kind, mem in (("all", None), ("ret", member)):
+            for i, (best, arg, other, cand) in enumerate(_brute_best(K.tolist(), mem, w)):
+                got = int(r["arg_" + kind][i])
+                assert abs(r["best_" + kind][i] - best) < 1e-12, (trial, kind, i)
+                if best - other > 1e-9:      # exact ties only: the smallest position
+                    assert got == arg, (trial, kind, i)
+                else:                        # a near-tie: any candidate within 1e-9 of the best
+                    assert got in cand and cand[got] >= best - 1e-9, (trial, kind, i)
+
+
 def pin_twin_counts_brute_force(o):
     rng = np.random.default_rng(11)
     for trial in range(6):
@@ -538,7 +593,7 @@ ALL_PINS = [
     pin_closed_forms, pin_window_and_sentinel, pin_scale_invariance, pin_bf16_decode,
     pin_nonfinite_rejected, pin_repair_ranked, pin_oscillation, pin_repair_invariants,
     pin_exact_noops, pin_redundancy_consistent_noop, pin_second_pass_condition,
-    pin_budget_checked,
+    pin_budget_checked, pin_nn_scores_brute_force,
     pin_twin_counts_golden, pin_twin_counts_band, pin_twin_counts_brute_force, pin_twin_counts_vs_best,
     pin_scores_eq3, pin_evict_golden, pin_evict_invariants, pin_prevalence_golden,
     pin_compact_golden, pin_compact_invariants, pin_exemption_diagnostics,
