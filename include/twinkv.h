@@ -110,7 +110,10 @@ int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs
  *
  * Similarities are computed from the stored key values with fp32 accumulation; their error
  * against exact arithmetic is below 1e-4 for bf16 and fp32 keys (this includes the rounding
- * down of reported values by less than the tie bound above).
+ * down of reported values by less than the tie bound above).  Every result is independent of
+ * a key's length as Eq. 1 is: scaling a key by a power of two changes no output bit, as long
+ * as its elements, their products with the other keys' elements and its norm stay in fp32's
+ * normal range (below 2^120 and above 2^-126 in magnitude).
  */
 int twinkv_nn_scores(const void* keys, int dtype, int d, int n_heads, int n_seqs,
                      const int64_t* cu_seqlens, int64_t head_stride, int64_t token_stride,

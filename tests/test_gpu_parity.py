@@ -124,6 +124,33 @@ def test_zero_and_scaled_keys():
     assert np.all(np.abs(gpu["best_all"][:, 400] - 1.0) < 1e-5)
 
 
+@pytest.mark.parametrize("d,dtype", [(64, "bf16"), (128, "bf16"), (64, "f32"), (128, "f32")])
+def test_power_of_two_key_scaling_changes_nothing(d, dtype):
+    """Eq. 1 does not depend on a key's length.  The kernels keep that exactly: every key
+    multiplied by its own power of two 2^e, e in [-40, 40] (all elements, their products and
+    the norms stay in fp32's normal range), gives the same scores, positions, S1 and counts
+    bit for bit, with and without the all-keys sweep and in count mode."""
+    batch = synth.make_batch(small_spec(3, [700, 1300], d, dtype, 32, 13, dup_frac=0.3))
+    g = np.random.default_rng(13)
+    e = g.integers(-40, 41, size=batch.keys.shape[:2])
+    if dtype == "bf16":
+        f = synth.bf16_to_f32(batch.keys)
+        scaled = synth.bf16_bits(np.ldexp(f, e[:, :, None]).astype(np.float32))
+        assert np.array_equal(synth.bf16_to_f32(scaled), np.ldexp(f, e[:, :, None]))  # exact
+    else:
+        scaled = np.ldexp(batch.keys, e[:, :, None]).astype(np.float32)
+    kt0, kt1 = to_device(batch.keys, dtype), to_device(scaled, dtype)
+    rt = mask_to_device(batch.retained)
+    for want_all in (True, False):
+        r0 = binding.repair(kt0, rt, batch.budget, 0.9, 32, 2, 3, batch.cu_seqlens, want_all=want_all)
+        r1 = binding.repair(kt1, rt, batch.budget, 0.9, 32, 2, 3, batch.cu_seqlens, want_all=want_all)
+        for k in r0:
+            assert np.array_equal(host(r0[k]).view(np.uint8), host(r1[k]).view(np.uint8)), (k, want_all)
+    c0 = binding.twin_counts(kt0, 0.9, 32, batch.cu_seqlens)
+    c1 = binding.twin_counts(kt1, 0.9, 32, batch.cu_seqlens)
+    assert np.array_equal(host(c0["counts"]), host(c1["counts"]))
+
+
 def test_nonfinite_key_status():
     import torch
     batch = synth.make_batch(small_spec(3, [200, 300], 64, "bf16", 32, 3))
