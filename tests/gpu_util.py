@@ -174,6 +174,54 @@ def check_repair(s1_gpu, stats_gpu, b_gpu, orc: dict, s0, tau: float, n_sink: in
             "cut_diff": cut_o + cut_d, "shift_diff": shift, "diff": int((s1g != s1o).sum()), "m": m_g}
 
 
+def check_every_row(keys_np, dtype: str, retained, cu, w: int, gpu: dict, tol: float = VALUE_BOUND) -> dict:
+    """Properties of the reported best twins that hold at any size (Sec. 3.2 Eq. 1 and the
+    window; Sec. 3.4 Eq. 4), checked on every row of every problem without the O(N^2 d)
+    oracle: a reported position lies outside the row's window (and in S0 for b), its
+    similarity (fp64, one dot product) equals the reported value within ``tol``, the sentinel
+    (-1, -1) appears exactly where no position qualifies, and, since sim(i, j) = sim(j, i),
+    a row reported as the best twin of another has a best value at least that large.
+    gpu holds host arrays [n_heads][T]: best_all, arg_all and, when retained is given,
+    best_ret, arg_ret.  Returns counts of the rows checked."""
+    H = keys_np.shape[0]
+    n_rows = n_none = 0
+    for h in range(H):
+        for s in range(len(cu) - 1):
+            a, e = int(cu[s]), int(cu[s + 1])
+            n = e - a
+            if n == 0:
+                continue
+            Kh = oracle.normalise(oracle.decode_keys(keys_np[h, a:e], dtype))
+            idx = np.arange(n)
+            kinds = [("all", np.ones(n, bool))]
+            if retained is not None:
+                kinds.append(("ret", retained[h, a:e].astype(bool)))
+            for kind, mem in kinds:
+                arg = np.asarray(gpu["arg_" + kind][h, a:e]).astype(np.int64)
+                best = np.asarray(gpu["best_" + kind][h, a:e]).astype(np.float64)
+                # members j with |i - j| > w exist iff the prefix counts outside the window are > 0
+                pc = np.concatenate([[0], np.cumsum(mem)])
+                lo_cnt = pc[np.clip(idx - w, 0, n)]
+                hi_cnt = pc[n] - pc[np.clip(idx + w + 1, 0, n)]
+                exists = (lo_cnt + hi_cnt) > 0
+                has = arg >= 0
+                assert np.array_equal(has, exists), f"{kind}: sentinel rows differ from rows without candidates"
+                assert np.all(best[~has] == -1.0), f"{kind}: sentinel value"
+                i, j = idx[has], arg[has]
+                assert np.all(j < n) and np.all(np.abs(i - j) > w), f"{kind}: position inside the window"
+                assert np.all(mem[j]), f"{kind}: position outside the set"
+                sim = np.einsum("ij,ij->i", Kh[i], Kh[j])
+                err = np.abs(sim - best[has])
+                assert err.size == 0 or err.max() <= tol, f"{kind}: value at the reported position off by {err.max()}"
+                n_rows += int(has.sum())
+                n_none += int((~has).sum())
+            ba = np.asarray(gpu["best_all"][h, a:e]).astype(np.float64)
+            aa = np.asarray(gpu["arg_all"][h, a:e]).astype(np.int64)
+            ok = aa >= 0
+            assert np.all(ba[aa[ok]] >= ba[ok] - 2 * tol), "a reported twin has a smaller best value"
+    return {"rows_with_candidate": n_rows, "rows_without": n_none}
+
+
 def record_exemptions(name: str, rec: dict) -> None:
     """Print one workload's exemption accounting and, when TWINKV_PARITY_RECORD names a file,
     append it there as a JSON line (the committed parity record is made from that file)."""

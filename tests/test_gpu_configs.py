@@ -3,7 +3,10 @@
 The GPU processes every problem of each workload in one call.  On every problem the oracle
 replays the repair logic of Sec. 3.4 on the GPU's own scores (bit for bit) and checks the
 set's properties; complete problems go through the full O(N^2 d) oracle and the token-by-token
-protocol of gpu_util; sampled rows of further problems check both reductions.  Each workload's
+protocol of gpu_util; sampled rows of further problems check both reductions; and every row
+of every problem is checked for what holds at any size (the reported position lies outside
+the window and in the right set, achieves the reported value, sentinels exactly where no
+position qualifies, and the symmetry of Eq. 1 between a row and its reported twin).  Each workload's
 exemption accounting (rows exempt by the runner-up margin, flags within the tolerance of tau,
 tokens at a selection cut) is printed and, with TWINKV_PARITY_RECORD set, recorded."""
 from concurrent.futures import ThreadPoolExecutor
@@ -12,8 +15,8 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import (check_repair, check_scores, host, mask_to_device, merge_repairs,
-                      merge_scores, record_exemptions, replay_repair, to_device)
+from gpu_util import (check_every_row, check_repair, check_scores, host, mask_to_device,
+                      merge_repairs, merge_scores, record_exemptions, replay_repair, to_device)
 from paper_2608_27128_amd import binding, synth
 
 pytestmark = pytest.mark.gpu
@@ -46,6 +49,12 @@ def check_all_problems(batch, out, tau, n_sink, n_recent):
             assert int(s1[h, a:e].sum()) == int(batch.budget[s])
             swapped += r["m"]
     return swapped
+
+
+def every_row(batch, out, w):
+    """check_every_row on the complete result: every row of every problem."""
+    g = {k: host(out[k]) for k in ("best_all", "arg_all", "best_ret", "arg_ret")}
+    return check_every_row(batch.keys, batch.dtype, batch.retained, batch.cu_seqlens, w, g)
 
 
 def check_sampled_rows(batch, out, problems, rng, w, agg=None):
@@ -106,7 +115,9 @@ def test_tiny_full_parity():
     swapped = check_all_problems(batch, out, sp.tau, sp.n_sink, sp.n_recent)
     res, agg = check_full_problems(batch, out, [(0, 0)], sp.tau, sp.n_sink, sp.n_recent)
     assert res[0][2]["exact"], "tiny: S1 differs from the oracle"
-    record_exemptions("tiny", {"problems_replayed": 1, "swapped": swapped, "full": agg})
+    rows = every_row(batch, out, sp.w)
+    record_exemptions("tiny", {"problems_replayed": 1, "swapped": swapped, "full": agg,
+                               "every_row": rows})
 
 
 @pytest.mark.timeout(600)
@@ -119,8 +130,9 @@ def test_llama1b_8k():
     sampled = check_sampled_rows(batch, out, [(0, 0), (77, 0), (127, 0)], rng, sp.w)
     res, agg = check_full_problems(batch, out, [(5, 0), (100, 0), (31, 0), (64, 0)], sp.tau,
                                    sp.n_sink, sp.n_recent)
+    rows = every_row(batch, out, sp.w)
     record_exemptions("llama1b_8k", {"problems_replayed": batch.n_heads, "swapped": swapped,
-                                     "sampled": sampled, "full": agg})
+                                     "sampled": sampled, "full": agg, "every_row": rows})
 
 
 @pytest.mark.timeout(900)
@@ -143,12 +155,14 @@ def test_qwen4b_16k_sweep(frac):
         if b_first is None:
             b_first = b
             sampled = check_sampled_rows(batch, out, [(3, 0), (200, 0)], rng, sp.w)
+            rows = every_row(batch, out, sp.w)
         else:
             assert np.array_equal(b, b_first), "b changed with tau"
         res, agg = check_full_problems(batch, out, full, tau, sp.n_sink, sp.n_recent, scores=scores)
         record_exemptions(f"qwen4b_16k budget {frac} tau {tau}",
                           {"problems_replayed": batch.n_heads, "swapped": swapped, "full": agg,
-                           **({"sampled": sampled} if tau == synth.QWEN_SWEEP_TAUS[0] else {})})
+                           **({"sampled": sampled, "every_row": rows}
+                              if tau == synth.QWEN_SWEEP_TAUS[0] else {})})
 
 
 @pytest.mark.timeout(900)
@@ -160,8 +174,9 @@ def test_long_aniso_32k():
     rng = np.random.default_rng(3)
     sampled = check_sampled_rows(batch, out, [(0, 0), (131, 0), (287, 0)], rng, sp.w)
     res, agg = check_full_problems(batch, out, [(17, 0), (202, 0)], sp.tau, sp.n_sink, sp.n_recent)
+    rows = every_row(batch, out, sp.w)
     record_exemptions("long_aniso_32k", {"problems_replayed": batch.n_heads, "swapped": swapped,
-                                         "sampled": sampled, "full": agg})
+                                         "sampled": sampled, "full": agg, "every_row": rows})
 
 
 @pytest.mark.timeout(900)
@@ -174,5 +189,6 @@ def test_ragged_64x_one_launch():
     shortest, longest = int(np.argmin(lens)), int(np.argmax(lens))
     probs = [(0, shortest), (287, longest), (100, 5), (9, 40), (150, 63), (222, 17)]
     res, agg = check_full_problems(batch, out, probs, sp.tau, sp.n_sink, sp.n_recent)
+    rows = every_row(batch, out, sp.w)
     record_exemptions("ragged_64x", {"problems_replayed": batch.n_heads * batch.n_seqs,
-                                     "swapped": swapped, "full": agg})
+                                     "swapped": swapped, "full": agg, "every_row": rows})

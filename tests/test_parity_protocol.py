@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import check_repair, check_scores
+from gpu_util import check_every_row, check_repair, check_scores
 
 
 def _problem(seed, n=400, d=16, tau=0.9, w=4):
@@ -143,3 +143,58 @@ def test_rank_error_beyond_tolerance_fails():
     b[24] += 0.015                            # 5e-3 past orphan 25: a rank error beyond tolerance
     with pytest.raises(AssertionError, match="cut"):
         run(b)
+
+
+def _every_row_case():
+    """Two ragged heads (an empty sequence, one shorter than the window) with the oracle's own
+    best twins in the [n_heads][T] layout check_every_row reads."""
+    rng = np.random.default_rng(5)
+    cu = np.array([0, 300, 300, 330, 336], np.int64)
+    H, T, d, w = 2, int(cu[-1]), 8, 4
+    K = rng.standard_normal((H, T, d)).astype(np.float32)
+    K[0, 40] = K[0, 10]                                  # an exact tie
+    ret = (rng.random((H, T)) < 0.5).astype(np.uint8)
+    ret[1, 330:336] = 0                                  # a sequence with an empty S0
+    g = {k: np.full((H, T), -1.0 if k.startswith("best") else -1) for k in
+         ("best_all", "arg_all", "best_ret", "arg_ret")}
+    for h in range(H):
+        for s in range(len(cu) - 1):
+            a, e = int(cu[s]), int(cu[s + 1])
+            if e > a:
+                r = oracle.nn_scores(K[h, a:e], "f32", ret[h, a:e], w)
+                for k in g:
+                    g[k][h, a:e] = r[k]
+    return K, ret, cu, w, g
+
+
+def test_every_row_check_accepts_the_oracle():
+    K, ret, cu, w, g = _every_row_case()
+    st = check_every_row(K, "f32", ret, cu, w, g)
+    assert st["rows_with_candidate"] > 1000 and st["rows_without"] > 0
+
+
+@pytest.mark.parametrize("mistake", ["moved", "in_window", "sentinel_with_candidates",
+                                     "candidate_without_members", "non_member", "value_off",
+                                     "asymmetric"])
+def test_every_row_check_rejects_planted_mistakes(mistake):
+    K, ret, cu, w, g = _every_row_case()
+    g = {k: v.copy() for k, v in g.items()}
+    i = int(np.nonzero(g["arg_all"][0, :300] >= 0)[0][7])
+    if mistake == "moved":                       # another position, far from a tie
+        g["arg_all"][0, i] = (g["arg_all"][0, i] + 97) % 300
+    elif mistake == "in_window":
+        g["arg_all"][0, i] = i + 1
+    elif mistake == "sentinel_with_candidates":
+        g["arg_ret"][0, i], g["best_ret"][0, i] = -1, -1.0
+    elif mistake == "candidate_without_members":     # sequence 3 of head 1 has no S0 member
+        g["arg_ret"][1, 331], g["best_ret"][1, 331] = 5, 0.0
+    elif mistake == "non_member":
+        j = int(np.nonzero(ret[0, :300] == 0)[0][-1])
+        g["arg_ret"][0, i] = j
+    elif mistake == "value_off":
+        g["best_all"][0, i] += 3e-4
+    else:                                        # the reported twin's own best made too small
+        j = int(g["arg_all"][0, i])
+        g["best_all"][0, j] = g["best_all"][0, i] - 1e-2
+    with pytest.raises(AssertionError):
+        check_every_row(K, "f32", ret, cu, w, g)
