@@ -178,18 +178,22 @@ thread_local hipEvent_t g_sim_stop = nullptr;
 struct Prepared {
   SimArgs args;         // everything but the outputs, w, want_all and the count mode
   SeqInfo* seqtab = nullptr;
+  int prep_blocks = 0;  // K1b workgroups per head
 };
 
+// K1a, K1b (unless key_prep is false: the level groups run one K1b for all their column
+// lists) and the similarity kernel's arguments for one column split.
 int prepare_scores(const void* keys, int dtype, int d, const Batch& bt, const int64_t* cu,
                    const int64_t* budget, int64_t head_stride, int64_t token_stride,
                    const uint8_t* retained, int32_t* status, char* ws, const Layout& L,
-                   bool copy_evicted, void* stream, Prepared& P) {
+                   bool copy_evicted, void* stream, Prepared& P, bool key_prep = true) {
   int total_tiles = 0;
   const int rpb = sim_rows_per_block(dtype, d);
   int64_t prep_blocks = 0;
   std::vector<SeqInfo> tab = seq_table(cu, bt.n_seqs, budget, rpb, total_tiles,
                                        prepare_tokens_per_block(dtype, d), &prep_blocks);
   if (prep_blocks > (int64_t)INT32_MAX) return TWINKV_E_ARG;
+  P.prep_blocks = (int)prep_blocks;
   const int64_t groups = bt.n_heads >= 8 ? 8LL * ((bt.n_heads + 7) / 8) : bt.n_heads;
   if (groups * total_tiles > (int64_t)INT32_MAX) return TWINKV_E_ARG;
 
@@ -209,10 +213,12 @@ int prepare_scores(const void* keys, int dtype, int d, const Batch& bt, const in
   int e = launch_partition(retained, dtab, bt.n_heads, bt.n_seqs, bt.T, bt.PT,
                            max_seq_len(cu, bt.n_seqs), pcol, rcol, prank, pmeta, status, stream);
   if (e) return hip_status(e);
-  e = launch_prepare_keys(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, bt.PT,
-                          (int)prep_blocks, retained, prank, pmeta, dtab, bt.n_seqs, rinv, rcol,
-                          hilo, pkeys, status, copy_evicted ? 1 : 0, stream);
-  if (e) return hip_status(e);
+  if (key_prep) {
+    e = launch_prepare_keys(keys, dtype, d, bt.n_heads, bt.T, head_stride, token_stride, bt.PT,
+                            (int)prep_blocks, retained, prank, pmeta, dtab, bt.n_seqs, rinv, rcol,
+                            hilo, pkeys, status, copy_evicted ? 1 : 0, stream);
+    if (e) return hip_status(e);
+  }
 
   SimArgs& a = P.args;
   if (dtype == TWINKV_F32) {
@@ -605,15 +611,33 @@ int twinkv_nn_scores_levels(const void* keys, int dtype, int d, int n_heads, int
   float* gbest = reinterpret_cast<float*>(base + LL.gbest);
   int32_t* garg = reinterpret_cast<int32_t*>(base + LL.garg);
 
-  // every group's partition and key preparation first, then the similarity sweeps back to back
+  // every group's partition, then one key preparation for all groups (the keys are read
+  // once; each goes to its own group's column list), then the similarity sweeps back to back
   Prepared P[kMaxLevels + 1];
   for (int g = 0; g < LL.groups; ++g) {
     const int sel = g < n_levels ? g + 1 : 0;  // the last group: the tokens in no set
     if (launch_select_level(level, mask, n, sel, n_levels, stream) != 0) return TWINKV_E_HIP;
     rc = prepare_scores(keys, dtype, d, bt, cu_seqlens, nullptr, head_stride, token_stride, mask,
                         g == 0 ? status : nullptr, base + LL.per * (size_t)g, L,
-                        /*copy_evicted=*/false, stream, P[g]);
+                        /*copy_evicted=*/false, stream, P[g], /*key_prep=*/false);
     if (rc != TWINKV_OK) return rc;
+  }
+  {
+    // group 0's arrays; group g's lie g * LL.per bytes further, at the same layout offsets
+    const PrepLevels lv{level, n_levels, LL.groups, (int64_t)LL.per};
+    const int e = launch_prepare_keys_levels(
+        keys, dtype, d, n_heads, bt.T, head_stride, token_stride, bt.PT, P[0].prep_blocks, lv,
+        reinterpret_cast<const int32_t*>(base + L.prank),
+        reinterpret_cast<ProblemMeta*>(base + L.pmeta), P[0].seqtab, n_seqs,
+        reinterpret_cast<float*>(base + L.rinv), reinterpret_cast<float*>(base + L.rcol),
+        dtype == TWINKV_F32 ? reinterpret_cast<uint16_t*>(base + L.hilo) : nullptr,
+        reinterpret_cast<uint16_t*>(base + L.pkeys), status, stream);
+    if (e) return hip_status(e);
+    // the rows' inverse norms (and the fp32 row plane) exist once, in group 0's slice
+    for (int g = 1; g < LL.groups; ++g) {
+      P[g].args.rinv = P[0].args.rinv;
+      if (dtype == TWINKV_F32) P[g].args.keys = P[0].args.keys;
+    }
   }
   if ((rc = record(g_sim_start, stream)) != TWINKV_OK) return rc;
   for (int g = 0; g < LL.groups; ++g) {

@@ -131,13 +131,18 @@ __device__ inline void prep_store16(uint16_t* p, uint4 x) {
   __builtin_nontemporal_store(v, reinterpret_cast<prep_u32x4*>(p));
 }
 
-template <int D, bool F32>
+// LEVELS: the groups of nested retained sets in one pass (PrepLevels): each token goes to
+// the column list of its own group, whose arrays lie group_stride bytes after the previous
+// group's; rinv (and the fp32 row plane) is written once for all groups.  Without LEVELS,
+// `retained` splits the positions into the one S0 list and the evicted list.
+template <int D, bool F32, bool LEVELS>
 __global__ __launch_bounds__(256) void prepare_keys_kernel(
     const uint8_t* __restrict__ keys, int64_t T, int64_t hs_bytes, int64_t ts_bytes, int64_t PT,
     const uint8_t* __restrict__ retained, const int32_t* __restrict__ prank,
     ProblemMeta* __restrict__ pmeta, const SeqInfo* __restrict__ seqtab, int n_seqs,
     float* __restrict__ rinv, float* __restrict__ rcol, uint16_t* __restrict__ hilo,
-    uint16_t* __restrict__ pkeys, int32_t* __restrict__ status, int h0, int copy_evicted) {
+    uint16_t* __restrict__ pkeys, int32_t* __restrict__ status, int h0, int copy_evicted,
+    PrepLevels lv) {
   constexpr int ESZ = F32 ? 4 : 2;
   constexpr int LPT = D * ESZ / 16;
   constexpr int TPB = 256 / LPT;
@@ -156,8 +161,8 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
   const int sub = threadIdx.x % LPT;
   const int tfirst = (bx - si.prep_blk0) * (TPB * kPrepIter) + threadIdx.x / LPT;
   const int64_t base = h * PT + si.perm_off;
-  const int ret_cols = pmeta[q].ret_chunks * kChunk;
-  const int n_ret = pmeta[q].n_ret;
+  const int ret_cols = LEVELS ? 0 : pmeta[q].ret_chunks * kChunk;
+  const int n_ret0 = LEVELS ? 0 : pmeta[q].n_ret;
 
   uint4 raw[kPrepIter];
 #pragma unroll
@@ -172,8 +177,20 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
     const int tl = tfirst + it * TPB;
     const bool valid = tl < si.len;
     const int64_t tt = si.start + (valid ? tl : 0);
-    const bool r = retained != nullptr && retained[h * T + tt] != 0;
-    const int pr = prank[base + (valid ? tl : 0)];
+    // this token's column list: its group's (LEVELS) or the single split's
+    int64_t goff = 0;
+    bool r;
+    int n_ret = n_ret0;
+    if constexpr (LEVELS) {
+      const int l = lv.level[h * T + tt];
+      const int g = (l >= 1 && l <= lv.n_levels) ? l - 1 : (lv.n_groups > lv.n_levels ? lv.n_levels : -1);
+      r = g >= 0;                      // a member of its group's list; else copied nowhere
+      goff = (int64_t)(r ? g : 0) * lv.group_stride;
+      n_ret = reinterpret_cast<const ProblemMeta*>(reinterpret_cast<const char*>(pmeta) + goff)[q].n_ret;
+    } else {
+      r = retained != nullptr && retained[h * T + tt] != 0;
+    }
+    const int pr = reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(prank) + goff)[base + (valid ? tl : 0)];
     const int p = r ? pr : ret_cols + ((valid ? tl : 0) - pr);
     const bool copy = valid && (r || copy_evicted);  // evicted columns only for all-keys sweeps
     // The last column of a group fills the rest of its 32-column chunk with copies of itself
@@ -181,6 +198,8 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
     // exact ties of a real column and the similarity sweep needs no padding test for it.
     const int last = r ? n_ret - 1 : ret_cols + (si.len - n_ret) - 1;
     const int fill_end = (p == last && copy) ? (p / kChunk + 1) * kChunk : p + 1;
+    uint16_t* const gkeys = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(pkeys) + goff);
+    float* const grcol = reinterpret_cast<float*>(reinterpret_cast<char*>(rcol) + goff);
 
     double ss = 0.0;
     if constexpr (F32) {
@@ -203,7 +222,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
         *reinterpret_cast<uint2*>(row) = phi;
         *reinterpret_cast<uint2*>(row + D) = plo;
         for (int k = p; copy && k < fill_end; ++k) {
-          uint16_t* dk = pkeys + (base + k) * DCOL;
+          uint16_t* dk = gkeys + (base + k) * DCOL;
           *reinterpret_cast<uint2*>(dk + sub * 4) = phi;
           *reinterpret_cast<uint2*>(dk + D + sub * 4) = plo;
         }
@@ -217,7 +236,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
         ss += x0 * x0 + x1 * x1;
       }
       for (int k = p; copy && k < fill_end; ++k)
-        prep_store16(pkeys + (base + k) * DCOL + sub * 8, raw[it]);
+        prep_store16(gkeys + (base + k) * DCOL + sub * 8, raw[it]);
     }
 #pragma unroll
     for (int off = LPT / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, LPT);
@@ -228,9 +247,13 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
       else if (ss > 0.0) rv = (float)(1.0 / sqrt(ss));
       else rv = 0.0f;                                       // zero key: similarity 0 to all
       rinv[h * T + tt] = rv;
-      for (int k = p; k < fill_end; ++k) rcol[base + k] = rv;
+      // (a token in no group of the LEVELS pass has no column anywhere)
+      for (int k = p; (copy || !LEVELS) && k < fill_end; ++k) grcol[base + k] = rv;
       if (bad) {
-        atomicOr(&pmeta[q].flags, kFlagNonfinite);
+        for (int g = 0; g < (LEVELS ? lv.n_groups : 1); ++g)  // every list of the problem
+          atomicOr(&reinterpret_cast<ProblemMeta*>(reinterpret_cast<char*>(pmeta) +
+                                                   (int64_t)g * lv.group_stride)[q].flags,
+                   kFlagNonfinite);
         if (status) status[q] = 2;  // TWINKV_PROBLEM_NONFINITE
       }
     }
@@ -242,24 +265,51 @@ constexpr int prep_tokens_per_block() {
   return 256 / (D * (F32 ? 4 : 2) / 16) * kPrepIter;
 }
 
-template <int D, bool F32>
+template <int D, bool F32, bool LEVELS>
 hipError_t run_prepare(const void* keys, int n_heads, int64_t T, int64_t hs, int64_t ts,
                        int64_t PT, int total_blocks, const uint8_t* retained, const int32_t* prank,
                        ProblemMeta* pmeta, const SeqInfo* seqtab, int n_seqs, float* rinv,
                        float* rcol, uint16_t* hilo, uint16_t* pkeys, int32_t* status,
-                       int copy_evicted, hipStream_t st) {
+                       int copy_evicted, const PrepLevels& lv, hipStream_t st) {
   constexpr int ESZ = F32 ? 4 : 2;
   if (total_blocks == 0 || n_heads == 0) return hipSuccess;
   for (int h0 = 0; h0 < n_heads; h0 += 65535) {  // heads along y, in slices the grid holds
     const int by = n_heads - h0 < 65535 ? n_heads - h0 : 65535;
-    hipLaunchKernelGGL((prepare_keys_kernel<D, F32>), dim3((unsigned)total_blocks, (unsigned)by),
-                       dim3(256), 0, st, (const uint8_t*)keys, T, hs * ESZ, ts * ESZ, PT,
-                       retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys, status,
-                       h0, copy_evicted);
+    hipLaunchKernelGGL((prepare_keys_kernel<D, F32, LEVELS>),
+                       dim3((unsigned)total_blocks, (unsigned)by), dim3(256), 0, st,
+                       (const uint8_t*)keys, T, hs * ESZ, ts * ESZ, PT, retained, prank, pmeta,
+                       seqtab, n_seqs, rinv, rcol, hilo, pkeys, status, h0, copy_evicted, lv);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+template <bool LEVELS>
+int prepare_dispatch(const void* keys, int dtype, int d, int n_heads, int64_t T,
+                     int64_t head_stride, int64_t token_stride, int64_t PT, int total_blocks,
+                     const uint8_t* retained, const int32_t* prank, ProblemMeta* pmeta,
+                     const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol, uint16_t* hilo,
+                     uint16_t* pkeys, int32_t* status, int copy_evicted, const PrepLevels& lv,
+                     void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == 0 && d == 64)
+    return run_prepare<64, false, LEVELS>(keys, n_heads, T, head_stride, token_stride, PT,
+                                          total_blocks, retained, prank, pmeta, seqtab, n_seqs,
+                                          rinv, rcol, hilo, pkeys, status, copy_evicted, lv, st);
+  if (dtype == 0 && d == 128)
+    return run_prepare<128, false, LEVELS>(keys, n_heads, T, head_stride, token_stride, PT,
+                                           total_blocks, retained, prank, pmeta, seqtab, n_seqs,
+                                           rinv, rcol, hilo, pkeys, status, copy_evicted, lv, st);
+  if (dtype == 1 && d == 64)
+    return run_prepare<64, true, LEVELS>(keys, n_heads, T, head_stride, token_stride, PT,
+                                         total_blocks, retained, prank, pmeta, seqtab, n_seqs,
+                                         rinv, rcol, hilo, pkeys, status, copy_evicted, lv, st);
+  if (dtype == 1 && d == 128)
+    return run_prepare<128, true, LEVELS>(keys, n_heads, T, head_stride, token_stride, PT,
+                                          total_blocks, retained, prank, pmeta, seqtab, n_seqs,
+                                          rinv, rcol, hilo, pkeys, status, copy_evicted, lv, st);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -294,24 +344,21 @@ int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t
                         const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
                         uint16_t* hilo, uint16_t* pkeys, int32_t* status, int copy_evicted,
                         void* stream) {
-  hipStream_t st = (hipStream_t)stream;
-  if (dtype == 0 && d == 64)
-    return run_prepare<64, false>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
-                                  retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                  status, copy_evicted, st);
-  if (dtype == 0 && d == 128)
-    return run_prepare<128, false>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
-                                   retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                   status, copy_evicted, st);
-  if (dtype == 1 && d == 64)
-    return run_prepare<64, true>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
-                                 retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                 status, copy_evicted, st);
-  if (dtype == 1 && d == 128)
-    return run_prepare<128, true>(keys, n_heads, T, head_stride, token_stride, PT, total_blocks,
-                                  retained, prank, pmeta, seqtab, n_seqs, rinv, rcol, hilo, pkeys,
-                                  status, copy_evicted, st);
-  return hipErrorInvalidValue;
+  const PrepLevels none{nullptr, 0, 1, 0};
+  return prepare_dispatch<false>(keys, dtype, d, n_heads, T, head_stride, token_stride, PT,
+                                 total_blocks, retained, prank, pmeta, seqtab, n_seqs, rinv, rcol,
+                                 hilo, pkeys, status, copy_evicted, none, stream);
+}
+
+int launch_prepare_keys_levels(const void* keys, int dtype, int d, int n_heads, int64_t T,
+                               int64_t head_stride, int64_t token_stride, int64_t PT,
+                               int total_blocks, const PrepLevels& lv, const int32_t* prank,
+                               ProblemMeta* pmeta, const SeqInfo* seqtab, int n_seqs, float* rinv,
+                               float* rcol, uint16_t* hilo, uint16_t* pkeys, int32_t* status,
+                               void* stream) {
+  return prepare_dispatch<true>(keys, dtype, d, n_heads, T, head_stride, token_stride, PT,
+                                total_blocks, nullptr, prank, pmeta, seqtab, n_seqs, rinv, rcol,
+                                hilo, pkeys, status, /*copy_evicted=*/0, lv, stream);
 }
 
 }  // namespace twinkv

@@ -75,6 +75,24 @@ int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t
                         const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
                         uint16_t* hilo, uint16_t* pkeys, int32_t* status, int copy_evicted,
                         void* stream);
+// K1b for the level groups of nested retained sets in one pass over the keys: a token of
+// level l in [1, n_levels] goes to the S0 list of group l - 1, a token of level 0 or above
+// n_levels to group n_levels when n_groups > n_levels (the tokens in no set) and nowhere
+// otherwise.  prank, pmeta, rcol and pkeys are group 0's; group g's lie g * group_stride
+// bytes further (each group partitioned by K1a beforehand).  rinv (and the fp32 row plane)
+// is written once.
+struct PrepLevels {
+  const uint8_t* level;   // [n_heads][T]
+  int n_levels;
+  int n_groups;
+  int64_t group_stride;   // bytes between consecutive groups' arrays
+};
+int launch_prepare_keys_levels(const void* keys, int dtype, int d, int n_heads, int64_t T,
+                               int64_t head_stride, int64_t token_stride, int64_t PT,
+                               int total_blocks, const PrepLevels& lv, const int32_t* prank,
+                               ProblemMeta* pmeta, const SeqInfo* seqtab, int n_seqs, float* rinv,
+                               float* rcol, uint16_t* hilo, uint16_t* pkeys, int32_t* status,
+                               void* stream);
 
 struct SimArgs {
   const void* keys;          // bf16 keys, or the hi/lo planes for fp32 keys

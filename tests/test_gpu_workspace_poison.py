@@ -93,3 +93,24 @@ def test_workspace_on_another_device_or_strided_is_refused():
     wide = torch.full(((nbytes + 3) // 4,), -1, dtype=torch.int32, device="cuda")
     got = binding.repair(*args, workspace=wide)
     same(ref, got, ["s1", "stats", "best_ret", "arg_ret", "best_all", "arg_all"])
+
+
+@pytest.mark.parametrize("H,lens,d,dtype,w", CASES)
+def test_levels_ignore_workspace_contents(H, lens, d, dtype, w):
+    """The nested-sets call (one key preparation for all level groups, each group's column
+    list in its own workspace slice) on a zeroed and on a poisoned workspace."""
+    import torch
+    batch = synth.make_batch(spec_of(H, lens, d, dtype, w, 5))
+    g = np.random.default_rng(5)
+    level = g.integers(0, 5, batch.retained.shape).astype(np.uint8)   # 4 = above n_levels
+    kt, cu = to_device(batch.keys, dtype), batch.cu_seqlens
+    lv = torch.from_numpy(level).cuda()
+    dt = 0 if dtype == "bf16" else 1
+    for want_all in (False, True):
+        nbytes = binding.levels_workspace_bytes(dt, d, H, cu, 3, want_all)
+        zero, poison = workspaces(nbytes)
+        a = binding.nn_scores_levels(kt, lv, 3, w, cu, want_all=want_all, workspace=zero)
+        b = binding.nn_scores_levels(kt, lv, 3, w, cu, want_all=want_all, workspace=poison)
+        same(a, b, [k for k in a if k != "status"] + ["status"])
+        vals = host(a["best_lvl"])
+        assert np.isfinite(vals).all()
