@@ -86,6 +86,30 @@ int launch_prepare_keys(const void* keys, int dtype, int d, int n_heads, int64_t
   return 0;
 }
 
+int launch_prepare_keys_levels(const void* keys, int dtype, int d, int n_heads, int64_t T,
+                               int64_t head_stride, int64_t token_stride, int64_t PT, int,
+                               const PrepLevels& lv, const int32_t* prank, ProblemMeta* pmeta,
+                               const SeqInfo* seqtab, int n_seqs, float* rinv, float* rcol,
+                               uint16_t* hilo, uint16_t* pkeys, int32_t*, void*) {
+  ++stub::g_launches;
+  const int64_t esz = dtype == 1 ? 4 : 2;
+  if (T > 0)
+    touch(keys, esz * ((int64_t)(n_heads - 1) * head_stride + (T - 1) * token_stride + d));
+  touch(lv.level, (int64_t)n_heads * T);
+  const int64_t dcol = dtype == 1 ? 2 * d : d;
+  touch(seqtab, (int64_t)sizeof(SeqInfo) * n_seqs);
+  touch_out(rinv, 4 * (int64_t)n_heads * T);
+  if (dtype == 1) touch_out(hilo, 2 * (int64_t)n_heads * T * dcol);
+  for (int g = 0; g < lv.n_groups; ++g) {  // each group's arrays, group_stride bytes apart
+    const int64_t off = (int64_t)g * lv.group_stride;
+    touch(reinterpret_cast<const char*>(prank) + off, 4 * (int64_t)n_heads * PT);
+    touch_out(reinterpret_cast<char*>(pmeta) + off, (int64_t)sizeof(ProblemMeta) * n_heads * n_seqs);
+    touch_out(reinterpret_cast<char*>(rcol) + off, 4 * (int64_t)n_heads * PT);
+    touch_out(reinterpret_cast<char*>(pkeys) + off, 2 * (int64_t)n_heads * PT * dcol);
+  }
+  return 0;
+}
+
 int sim_rows_per_block(int dtype, int d) {
   if (dtype == 0) return d == 128 ? 384 : 512;
   return 128;
