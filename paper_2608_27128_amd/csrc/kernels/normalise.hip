@@ -10,6 +10,8 @@
 // (+5 bytes of mask and rank) and writes d*2 (+4d for fp32) + 8 bytes per key.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "../twinkv_internal.h"
 
 namespace twinkv {
@@ -122,6 +124,13 @@ constexpr int kPrepIter = 4;
 
 typedef unsigned int prep_u32x4 __attribute__((ext_vector_type(4)));
 
+// p moved by a byte offset (one level group's array from group 0's)
+template <typename T>
+__device__ inline T* byte_offset(T* p, int64_t bytes) {
+  using C = typename std::conditional<std::is_const<T>::value, const char, char>::type;
+  return reinterpret_cast<T*>(reinterpret_cast<C*>(p) + bytes);
+}
+
 __device__ inline uint4 prep_load16(const uint8_t* p) {
   const prep_u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const prep_u32x4*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);
@@ -183,14 +192,15 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
     int n_ret = n_ret0;
     if constexpr (LEVELS) {
       const int l = lv.level[h * T + tt];
-      const int g = (l >= 1 && l <= lv.n_levels) ? l - 1 : (lv.n_groups > lv.n_levels ? lv.n_levels : -1);
+      const int g = (l >= 1 && l <= lv.n_levels) ? l - 1
+                    : (lv.n_groups > lv.n_levels ? lv.n_levels : -1);
       r = g >= 0;                      // a member of its group's list; else copied nowhere
       goff = (int64_t)(r ? g : 0) * lv.group_stride;
-      n_ret = reinterpret_cast<const ProblemMeta*>(reinterpret_cast<const char*>(pmeta) + goff)[q].n_ret;
+      n_ret = byte_offset(pmeta, goff)[q].n_ret;
     } else {
       r = retained != nullptr && retained[h * T + tt] != 0;
     }
-    const int pr = reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(prank) + goff)[base + (valid ? tl : 0)];
+    const int pr = byte_offset(prank, goff)[base + (valid ? tl : 0)];
     const int p = r ? pr : ret_cols + ((valid ? tl : 0) - pr);
     const bool copy = valid && (r || copy_evicted);  // evicted columns only for all-keys sweeps
     // The last column of a group fills the rest of its 32-column chunk with copies of itself
@@ -198,8 +208,8 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
     // exact ties of a real column and the similarity sweep needs no padding test for it.
     const int last = r ? n_ret - 1 : ret_cols + (si.len - n_ret) - 1;
     const int fill_end = (p == last && copy) ? (p / kChunk + 1) * kChunk : p + 1;
-    uint16_t* const gkeys = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(pkeys) + goff);
-    float* const grcol = reinterpret_cast<float*>(reinterpret_cast<char*>(rcol) + goff);
+    uint16_t* const gkeys = byte_offset(pkeys, goff);
+    float* const grcol = byte_offset(rcol, goff);
 
     double ss = 0.0;
     if constexpr (F32) {
@@ -251,9 +261,7 @@ __global__ __launch_bounds__(256) void prepare_keys_kernel(
       for (int k = p; (copy || !LEVELS) && k < fill_end; ++k) grcol[base + k] = rv;
       if (bad) {
         for (int g = 0; g < (LEVELS ? lv.n_groups : 1); ++g)  // every list of the problem
-          atomicOr(&reinterpret_cast<ProblemMeta*>(reinterpret_cast<char*>(pmeta) +
-                                                   (int64_t)g * lv.group_stride)[q].flags,
-                   kFlagNonfinite);
+          atomicOr(&byte_offset(pmeta, (int64_t)g * lv.group_stride)[q].flags, kFlagNonfinite);
         if (status) status[q] = 2;  // TWINKV_PROBLEM_NONFINITE
       }
     }
