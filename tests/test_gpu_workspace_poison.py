@@ -114,3 +114,30 @@ def test_levels_ignore_workspace_contents(H, lens, d, dtype, w):
         same(a, b, [k for k in a if k != "status"] + ["status"])
         vals = host(a["best_lvl"])
         assert np.isfinite(vals).all()
+
+
+def test_concurrent_calls_on_two_streams():
+    """Calls with different workspaces may overlap (nothing else is shared between calls):
+    two batches repaired at the same time on two streams give what they give one after the
+    other, bit for bit."""
+    import torch
+    b1 = synth.make_batch(spec_of(9, [2100, 389], 128, "bf16", 32, 21))
+    b2 = synth.make_batch(spec_of(3, [1500, 700, 0, 33], 128, "bf16", 32, 22))
+    args = []
+    for b in (b1, b2):
+        sp = b.spec
+        args.append((to_device(b.keys, "bf16"), mask_to_device(b.retained), b.budget, sp.tau,
+                     sp.w, sp.n_sink, sp.n_recent, b.cu_seqlens))
+    ref = [binding.repair(*a) for a in args]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    got = [None, None]
+    for rep in range(3):
+        for i, (s, a) in enumerate(zip(streams, args)):
+            with torch.cuda.stream(s):
+                got[i] = binding.repair(*a)
+        torch.cuda.synchronize()
+        for r, g in zip(ref, got):
+            same(r, g, ["s1", "stats", "best_ret", "arg_ret", "best_all", "arg_all"])
