@@ -107,6 +107,8 @@ int64_t twinkv_workspace_bytes(int op, int dtype, int d, int n_heads, int n_seqs
  *              Nullable; must be NULL when retained is NULL.
  *   arg_ret    [n_heads][T] int32: the maximising retained j, -1 if none.  Nullable.
  *   status     [n_heads * n_seqs] int32 TWINKV_PROBLEM_* (only OK / NONFINITE).  Nullable.
+ *              The scores of a problem with a non-finite key are unspecified (the similarity
+ *              is undefined there); every other problem's are unaffected.
  *
  * Similarities are computed from the stored key values with fp32 accumulation; their error
  * against exact arithmetic is below 1e-4 for bf16 and fp32 keys (this includes the rounding

@@ -101,3 +101,29 @@ def test_levels_full_qwen4b_16k():
             gpu = {"best_ret": host(out["best_lvl"][k])[h], "arg_ret": host(out["arg_lvl"][k])[h]}
             orc_ret = {kk: v for kk, v in orc.items() if kk.endswith("_ret")}
             check_scores(gpu, orc_ret, rows, keys[h], "bf16", sets[k].retained[h], sp.w)
+
+
+def test_levels_nonfinite_key_flags_every_group():
+    """A NaN key: the problem's status is NONFINITE once (its scores are unspecified), and
+    every other problem's levels (and all-keys result) equal the separate single-set calls'
+    bit for bit."""
+    sets, keys, level = nested_batch(small(3, [700, 300], 128, "bf16", 8))
+    keys = keys.copy()
+    keys[1, 750, 5] = 0x7FC0                    # NaN in head 1, sequence 1
+    cu = sets[0].cu_seqlens
+    kt = to_device(keys, "bf16")
+    out = binding.nn_scores_levels(kt, mask_to_device(level), 3, 32, cu, want_all=True)
+    st = host(out["status"]).reshape(3, 2)
+    assert st[1, 1] == binding.PROBLEM_NONFINITE and st.sum() == binding.PROBLEM_NONFINITE
+    good = np.ones(keys.shape[:2], bool)
+    good[1, cu[1]:cu[2]] = False               # the flagged problem
+    for k in range(3):
+        ref = binding.nn_scores(kt, mask_to_device(sets[k].retained), 32, cu)
+        assert host(ref["status"]).reshape(3, 2)[1, 1] == binding.PROBLEM_NONFINITE
+        assert np.array_equal(host(out["best_lvl"][k]).view(np.uint32)[good],
+                              host(ref["best_ret"]).view(np.uint32)[good]), k
+        assert np.array_equal(host(out["arg_lvl"][k])[good], host(ref["arg_ret"])[good]), k
+        if k == 0:
+            assert np.array_equal(host(out["best_all"]).view(np.uint32)[good],
+                                  host(ref["best_all"]).view(np.uint32)[good])
+            assert np.array_equal(host(out["arg_all"])[good], host(ref["arg_all"])[good])
