@@ -190,6 +190,7 @@ int twinkv_repair_from_scores_noalloc(const float* b, const uint8_t* retained_in
  *   tau      twin threshold (finite).
  *   counts   [n_heads][T] int32 (required).
  *   status   [n_heads * n_seqs] int32 TWINKV_PROBLEM_* (only OK / NONFINITE).  Nullable.
+ *            The counts of a problem with a non-finite key are unspecified.
  *   workspace  twinkv_workspace_bytes(TWINKV_OP_TWIN_COUNTS, ...) bytes.
  *
  * The decision sim > tau is taken on fp32 similarities (error below 1e-4, typically 1e-6):
@@ -246,6 +247,8 @@ int64_t twinkv_levels_workspace_bytes(int dtype, int d, int n_heads, int n_seqs,
  *   scores        [n_heads][T] fp32, the Eq. 3 scores.  Nullable.
  *   stats         [n_heads * n_seqs][4] int32 = {tokens kept, count at the cut (-1 when the
  *                 cut falls inside the protected regions or nothing is cut), status, 0}.
+ *                 A problem with a non-finite key (status NONFINITE) still keeps exactly its
+ *                 budget, protected regions first; which other tokens is unspecified.
  *   workspace     twinkv_workspace_bytes(TWINKV_OP_SCORE_EVICT, ...) bytes.
  * Other arguments as in twinkv_twin_counts.
  */

@@ -206,3 +206,30 @@ def test_twin_counts_full_llama1b_8k():
         n += len(rows)
         exact += int((g == o["counts"]).sum())
     print("llama1b_8k twin counts: sampled rows", n, "exact", exact)
+
+
+def test_nonfinite_key_in_counts_and_eviction():
+    """A NaN key: its problem is flagged (twin counts and the scorer), the scorer still keeps
+    exactly its budget there with the protected regions first, and every other problem's
+    counts and kept set equal those of the same batch without the NaN, bit for bit."""
+    batch = synth.make_batch(small_spec(3, [400, 300], 128, "bf16", 16, 43))
+    clean = to_device(batch.keys, "bf16")
+    keys = batch.keys.copy()
+    keys[2, 500, 9] = 0x7FC0                   # NaN in head 2, sequence 1
+    dirty = to_device(keys, "bf16")
+    cu = batch.cu_seqlens
+    good = np.ones(keys.shape[:2], bool)
+    good[2, cu[1]:cu[2]] = False
+    c0 = binding.twin_counts(clean, 0.9, 16, cu)
+    c1 = binding.twin_counts(dirty, 0.9, 16, cu)
+    assert host(c1["status"]).reshape(3, 2).tolist() == [[0, 0], [0, 0], [0, 2]]
+    assert np.array_equal(host(c0["counts"])[good], host(c1["counts"])[good])
+    budget = np.array([150, 120], np.int64)
+    e0 = binding.score_evict(clean, budget, 0.9, 16, 4, 8, cu)
+    e1 = binding.score_evict(dirty, budget, 0.9, 16, 4, 8, cu)
+    st = host(e1["stats"]).reshape(3, 2, 4)
+    assert st[2, 1, 2] == 2 and st[:, :, 2].sum() == 2
+    k0, k1 = host(e0["retained"]), host(e1["retained"])
+    assert np.array_equal(k0[good], k1[good])
+    bad = k1[2, cu[1]:cu[2]]
+    assert bad.sum() == 120 and bad[:4].all() and bad[-8:].all()
