@@ -163,6 +163,31 @@ def test_nonfinite_key_status():
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_nonfinite_key_repair_keeps_s0(d):
+    """The repair of a problem with a NaN key leaves S1 = S0 with status NONFINITE (R4); every
+    other problem's S1, counts and scores equal those of the same batch without the NaN."""
+    batch = synth.make_batch(small_spec(3, [500, 700], d, "bf16", 32, 17))
+    cu = batch.cu_seqlens
+    keys = batch.keys.copy()
+    keys[0, 900, 3] = 0x7FC0           # NaN in head 0, sequence 1
+    rt = mask_to_device(batch.retained)
+    args = (batch.budget, 0.9, 32, 2, 3, cu)
+    r0 = binding.repair(to_device(batch.keys, "bf16"), rt, *args)
+    r1 = binding.repair(to_device(keys, "bf16"), rt, *args)
+    st = host(r1["stats"]).reshape(3, 2, 4)
+    assert st[0, 1, 3] == binding.PROBLEM_NONFINITE and st[:, :, 3].sum() == binding.PROBLEM_NONFINITE
+    s1 = host(r1["s1"])
+    assert np.array_equal(s1[0, cu[1]:cu[2]], batch.retained[0, cu[1]:cu[2]])
+    good = np.ones(keys.shape[:2], bool)
+    good[0, cu[1]:cu[2]] = False
+    for k in ("s1", "best_ret", "arg_ret", "best_all", "arg_all"):
+        assert np.array_equal(host(r0[k])[good].view(np.uint8), host(r1[k])[good].view(np.uint8)), k
+    st0 = host(r0["stats"]).reshape(3, 2, 4)
+    st0[0, 1], st[0, 1] = 0, 0
+    assert np.array_equal(st0, st)
+
+
 def test_deterministic():
     batch = synth.make_batch(small_spec(9, [1000, 1200], 128, "bf16", 32, 5))
     kt, rt = to_device(batch.keys, "bf16"), mask_to_device(batch.retained)
