@@ -163,14 +163,15 @@ def test_nonfinite_key_status():
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("d", [64, 128])
-def test_nonfinite_key_repair_keeps_s0(d):
-    """The repair of a problem with a NaN key leaves S1 = S0 with status NONFINITE (R4); every
-    other problem's S1, counts and scores equal those of the same batch without the NaN."""
+@pytest.mark.parametrize("d,bits", [(64, 0x7FC0), (128, 0x7FC0), (128, 0x7F80), (64, 0xFF80)],
+                         ids=["64-nan", "128-nan", "128-inf", "64-neg_inf"])
+def test_nonfinite_key_repair_keeps_s0(d, bits):
+    """The repair of a problem with a NaN or infinite key leaves S1 = S0 with status NONFINITE
+    (R4); every other problem's S1, counts and scores equal those of the same batch without it."""
     batch = synth.make_batch(small_spec(3, [500, 700], d, "bf16", 32, 17))
     cu = batch.cu_seqlens
     keys = batch.keys.copy()
-    keys[0, 900, 3] = 0x7FC0           # NaN in head 0, sequence 1
+    keys[0, 900, 3] = bits             # in head 0, sequence 1
     rt = mask_to_device(batch.retained)
     args = (batch.budget, 0.9, 32, 2, 3, cu)
     r0 = binding.repair(to_device(batch.keys, "bf16"), rt, *args)
